@@ -1,0 +1,244 @@
+#!/usr/bin/env python3
+"""Benchmark of the fused y = A^T (A x) on one MI355X (gfx950).
+
+A step is one mep_ata_x call over the 16384 x 16384 workload (uniform[-1,1)
+from seed 3): the matrix-streaming kernel (row dot + transposed accumulation
+in one read of A) and the fixed-order column reduction.  Inputs are resident
+in HBM before timing starts.  One JSON line is printed:
+
+* value     -- whole-job throughput, algorithmic bytes (A + x + y) per second
+* roofline  -- the streaming kernel's algorithmic bytes (A + x) divided by its
+               average duration, from HIP events recorded around every launch
+               of the timed region on the kernel's own stream
+* cpu_baseline -- the CPU oracle, as it stands, on the host cores
+
+Usage: python bench.py [--steps K] [--warmup W] [--dtype f32|f64]
+                       [--no-cpu-baseline] [--no-f64] [--probe-copy]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "achieved HBM GB/s (and % of MI355X peak) for y=Aᵀ(Ax), fp32 16384²"
+PEAK_GBS = 8000.0
+WORKLOAD = "ata_x_16384"
+KERNEL_SOURCES = ["paper_2512_22147_amd/csrc/mep_kernels.hpp",
+                  "paper_2512_22147_amd/csrc/mep_launch.inc",
+                  "paper_2512_22147_amd/csrc/mep_internal.hpp"]
+TRAFFIC_FILE = "profiles/ata_x_16384_traffic.md"
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(dtype: str):
+    """HBM bytes per launch of the streaming kernel from the committed
+    rocprofv3 counter summary, or None when absent or taken on other code."""
+    path = os.path.join(ROOT, TRAFFIC_FILE)
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m = re.search(r"kernel_source_sha256_16:\s*([0-9a-f]+)", text)
+    if not m or m.group(1) != kernel_source_hash():
+        return None
+    m = re.search(rf"traffic_bytes_per_launch_{dtype}:\s*([0-9.eE+]+)", text)
+    return float(m.group(1)) if m else None
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--dtype", choices=["f32", "f64"], default="f32")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-f64", action="store_true", help="skip the fp64 secondary measurement")
+    ap.add_argument("--probe-copy", action="store_true",
+                    help="also run the 1 GiB streaming-copy probe (counter calibration)")
+    ap.add_argument("--variant", type=int, default=-1, help="kernel candidate (Eqs. 4-5); -1 default")
+    return ap.parse_args()
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def run_gpu(dtype: str, steps: int, warmup: int, variant: int):
+    import numpy as np
+    import torch
+
+    from paper_2512_22147_amd import datagen, mep
+
+    npdt = np.float32 if dtype == "f32" else np.float64
+    w = datagen.WORKLOADS[WORKLOAD]
+    m, n = w.m, w.n
+    es = np.dtype(npdt).itemsize
+    log(f"[bench] generating {WORKLOAD} {dtype} ({m}x{n}, seed {w.seed})")
+    ins = datagen.make_inputs(w, npdt)
+    dev = torch.device("cuda:0")
+    A = torch.from_numpy(ins["A"]).to(dev)
+    x = torch.from_numpy(ins["x"]).to(dev)
+    y = torch.empty(n, dtype=A.dtype, device=dev)
+    need = mep.mep_workspace_bytes(mep.MEP_OP_ATA_X, mep.dtype_code(A.dtype), m, n)
+    ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    mep.mep_set_variant(mep.MEP_OP_ATA_X, variant)
+    stream = torch.cuda.current_stream()
+    log(f"[bench] warmup {warmup} steps")
+    for _ in range(warmup):
+        mep.mep_ata_x(A, x, y=y, ws=ws, stream=stream)
+    torch.cuda.synchronize()
+    mep.mep_profile_begin(steps)
+    log(f"[bench] timing {steps} steps")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        mep.mep_ata_x(A, x, y=y, ws=ws, stream=stream)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    kern_ms, launches = mep.mep_profile_end()
+    mep.mep_set_variant(mep.MEP_OP_ATA_X, -1)
+    alg_step = (m * n + n + n) * es          # A, x, y once
+    alg_kernel = (m * n + n) * es            # what the streaming kernel must read
+    ms_step = elapsed * 1e3 / steps
+    kavg_ms = kern_ms / max(launches, 1)
+    res = {
+        "dtype": dtype, "m": m, "n": n, "ms_per_step": ms_step,
+        "value_gbs": alg_step / (ms_step * 1e-3) / 1e9,
+        "kernel_ms": kavg_ms, "kernel_launches": launches,
+        "kernel_gbs": alg_kernel / (kavg_ms * 1e-3) / 1e9,
+        "alg_bytes_step": alg_step, "alg_bytes_kernel": alg_kernel,
+        "y": y.cpu().numpy(), "A_host": ins["A"], "x_host": ins["x"],
+    }
+    del A, x, y, ws
+    torch.cuda.empty_cache()
+    return res
+
+
+def probe_copy():
+    import torch
+
+    from paper_2512_22147_amd import mep
+
+    dev = torch.device("cuda:0")
+    nbytes = 1 << 30
+    src = torch.empty(nbytes, dtype=torch.uint8, device=dev).fill_(1)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        mep.mep_stream_copy(src, dst)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    reps = 10
+    for _ in range(reps):
+        mep.mep_stream_copy(src, dst)
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / reps
+    log(f"[bench] copy probe: {nbytes} B read + {nbytes} B written per launch, "
+        f"{2 * nbytes / dt / 1e9:.1f} GB/s")
+    return {"bytes_read": nbytes, "bytes_written": nbytes, "gbs": 2 * nbytes / dt / 1e9}
+
+
+def cpu_baseline(A_host, x_host, alg_bytes):
+    import numpy as np
+
+    import oracle
+
+    A64 = np.ascontiguousarray(A_host, dtype=np.float64)
+    x64 = np.ascontiguousarray(x_host, dtype=np.float64)
+    R, k = 3, 1
+    times = []
+    y = None
+    log(f"[bench] CPU oracle: {R} calls on {oracle.default().num_threads()} threads")
+    for _ in range(R):
+        t0 = time.perf_counter()
+        y, _ = oracle.ata_x(A64, x64)
+        times.append(time.perf_counter() - t0)
+    t = oracle.trimmed_mean(times, k)
+    return {
+        "value": alg_bytes / t / 1e9, "unit": "GB/s", "cores": oracle.default().num_threads(),
+        "kind": "oracle", "seconds_per_call": t,
+        "sample": f"the full {A_host.shape[0]}x{A_host.shape[1]} {A_host.dtype} workload (inputs promoted "
+                  f"to fp64 before timing), {R} calls, Eq. 3 trimmed mean with k={k}",
+    }, y
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the row-sharded "
+              "multi-GPU layout is a design, not a measured configuration", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    from paper_2512_22147_amd import mep
+
+    mep.lib()
+    prim = run_gpu(args.dtype, args.steps, args.warmup, args.variant)
+    fe = None
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu, yref = cpu_baseline(prim["A_host"], prim["x_host"], prim["alg_bytes_step"])
+        fe = mep.mep_check_fe(prim["y"], yref, 1e-4 if args.dtype == "f32" else 1e-12)[0]
+    secondary = None
+    if not args.no_f64 and args.dtype == "f32":
+        del prim["A_host"]
+        sec = run_gpu("f64", args.steps, args.warmup, args.variant)
+        secondary = {
+            "dtype": "f64", "value": round(sec["value_gbs"], 1), "unit": "GB/s",
+            "ms_per_step": round(sec["ms_per_step"], 4),
+            "kernel_gbs": round(sec["kernel_gbs"], 1),
+            "frac_of_peak": round(sec["kernel_gbs"] / PEAK_GBS, 4),
+            "traffic": measured_traffic("f64"),
+        }
+    copy = probe_copy() if args.probe_copy else None
+    traffic = measured_traffic(args.dtype)
+    out = {
+        "metric": METRIC,
+        "value": round(prim["value_gbs"], 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(prim["ms_per_step"], 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": args.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"y = A^T (A x), A {prim['m']}x{prim['n']} uniform[-1,1) seed 3",
+                   "m": prim["m"], "n": prim["n"], "seed": 3, "kernel_candidate": args.variant},
+        "pct_of_peak": round(100.0 * prim["value_gbs"] / PEAK_GBS, 2),
+        "roofline": {
+            "bound": "hbm", "achieved": round(prim["kernel_gbs"], 1), "peak": PEAK_GBS, "unit": "GB/s",
+            "frac": round(prim["kernel_gbs"] / PEAK_GBS, 4), "traffic": traffic,
+            "kernel": "k_stream (ATAX mode)", "kernel_ms": round(prim["kernel_ms"], 5),
+            "alg_bytes_per_launch": prim["alg_bytes_kernel"],
+        },
+        "cpu_baseline": cpu,
+        "fe_error_vs_oracle": fe,
+        "secondary": secondary,
+        "copy_probe": copy,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

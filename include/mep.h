@@ -1,0 +1,213 @@
+/*
+ * mep.h -- C-ABI of libmep.so: the dense matrix-vector family on MI355X
+ * (gfx950), wrapped in the minimal-executable-program (MEP) harness of
+ * "GPU Kernel Optimization Beyond Full Builds: An LLM Framework with Minimal
+ * Executable Programs" (arXiv 2512.22147).
+ *
+ * The paper's benchmark tables (Tables 1-2, Sec. 4.2) name the PolyBench
+ * kernels ATAX, BICG and GESUMMV; their computations are the matrix-vector
+ * products below.  The harness follows Sec. 3.1-3.2: a fixed problem size,
+ * repeated timed runs ranked by the trimmed mean of Eq. 3, and the
+ * functional-equivalence (FE) check of Eq. 4.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Matrices are row-major and contiguous: element (i, j) of the m x n
+ *   matrix A is A[i * n + j].  Vectors are contiguous.
+ * - dtype is MEP_F32 or MEP_F64.  Every vector has that element type and the
+ *   arithmetic is done in it (fp32 inputs accumulate in fp32).
+ * - Device pointers are plain HIP device addresses (e.g. a torch tensor's
+ *   data_ptr()).  Each must be aligned to its element size.  16-byte aligned
+ *   matrices whose row length is a multiple of 16 bytes take the 16-byte
+ *   vector path; anything else takes the element-wise path.  Both give
+ *   results within the same tolerance; each is deterministic.
+ * - 0 <= m <= 2^30 and 0 <= n <= 65535 * 8192.  A zero-length vector may be NULL.  An empty sum is
+ *   zero: e.g. with n = 0, y = A x is all zeros.
+ * - stream is a hipStream_t (NULL = the default stream).  Operations only
+ *   enqueue work and return; they never synchronize.
+ * - ws is a caller-owned device workspace of at least
+ *   mep_workspace_bytes(op, dtype, m, n) bytes (may be NULL when that is 0).
+ *   Its contents on entry are irrelevant and on exit unspecified.
+ * - Ownership: the caller allocates and frees every buffer.  The library
+ *   never allocates or frees device memory and keeps no pointer after a call
+ *   returns.
+ * - Errors: every argument is checked before anything is launched.  A
+ *   non-zero MEP_E* code means nothing was launched and nothing written;
+ *   mep_last_error() then describes the problem.  Outputs must not overlap
+ *   inputs, the workspace or each other.
+ * - Results are bitwise reproducible for a given binary, device, shape and
+ *   input: every reduction runs in a fixed order and no atomics are used.
+ */
+#ifndef MEP_H
+#define MEP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { MEP_F32 = 0, MEP_F64 = 1 } mep_dtype_t;
+
+enum {
+    MEP_OK = 0,
+    MEP_EINVAL = 1,      /* bad size, NULL pointer, overlap, bad op/dtype      */
+    MEP_EALIGN = 2,      /* pointer not aligned to its element size            */
+    MEP_EWORKSPACE = 3,  /* ws_bytes smaller than mep_workspace_bytes(...)     */
+    MEP_EHIP = 4,        /* the HIP runtime reported an error on launch        */
+    MEP_EBUDGET = 5      /* harness: R <= 2k or another budget violation       */
+};
+
+/* Operation codes, used by mep_workspace_bytes() and mep_call_t. */
+enum {
+    MEP_OP_MATVEC = 0,   /* y = A x                                          */
+    MEP_OP_MATVEC_T = 1, /* z = A^T w                                        */
+    MEP_OP_BICG = 2,     /* q = A p and s = A^T r, one read of A (BICG)      */
+    MEP_OP_ATA_X = 3,    /* y = A^T (A x) (ATAX)                             */
+    MEP_OP_AXPBY_MV = 4  /* y = alpha A x + beta B x (GESUMMV)               */
+};
+
+typedef void* mep_stream_t; /* hipStream_t */
+
+/* Workspace bytes that op needs for an m x n problem of the given dtype. */
+size_t mep_workspace_bytes(int op, int dtype, int64_t m, int64_t n);
+
+/*
+ * y = A x (matrix-vector product; the building block of ATAX, BICG and
+ * GESUMMV in Tables 1-2).  A: m x n, x: n, y: m.
+ */
+int mep_matvec(int dtype, int64_t m, int64_t n, const void* A, const void* x, void* y,
+               void* ws, size_t ws_bytes, mep_stream_t stream);
+
+/*
+ * z = A^T w (transposed product).  A: m x n, w: m, z: n.
+ * If p is not NULL, also q = A p (p: n, q: m) in the same single read of A:
+ * this pair is the BICG kernel of Tables 1-2 (q = A p, s = A^T r with w = r,
+ * z = s).  The pair is requested when p or q is non-NULL; then each of them
+ * may be NULL only if its length is zero.
+ */
+int mep_matvec_t(int dtype, int64_t m, int64_t n, const void* A, const void* w, void* z,
+                 const void* p, void* q, void* ws, size_t ws_bytes, mep_stream_t stream);
+
+/*
+ * y = A^T (A x): the ATAX kernel of Table 1.  A: m x n, x: n, y: n.
+ * t (nullable, length m) receives the intermediate A x.  When a row of A fits
+ * on chip (n <= 32768 for fp32, n <= 16384 for fp64, on the vector path) A is
+ * read from memory once; otherwise A x is formed first and A is read twice.
+ */
+int mep_ata_x(int dtype, int64_t m, int64_t n, const void* A, const void* x, void* y,
+              void* t, void* ws, size_t ws_bytes, mep_stream_t stream);
+
+/*
+ * y = alpha A x + beta B x: the GESUMMV kernel of Tables 1-2.  A, B: m x n,
+ * x: n, y: m.  On the fp32 path alpha and beta are rounded to fp32 first.
+ */
+int mep_axpby_mv(int dtype, int64_t m, int64_t n, double alpha, const void* A, double beta,
+                 const void* B, const void* x, void* y, void* ws, size_t ws_bytes,
+                 mep_stream_t stream);
+
+/*
+ * One operation, as the MEP harness runs it.  Field use per op:
+ *   MATVEC    in0 = x, out0 = y
+ *   MATVEC_T  in0 = w, out0 = z
+ *   BICG      in0 = r, out0 = s, in1 = p, out1 = q
+ *   ATA_X     in0 = x, out0 = y, out1 = t (nullable)
+ *   AXPBY_MV  A, B, in0 = x, out0 = y, alpha, beta
+ * flush_buf / flush_bytes: optional device buffer the harness overwrites
+ * before every timed sample so that no operand stays in the caches.
+ */
+typedef struct {
+    int op;
+    int dtype;
+    int64_t m, n;
+    const void* A;
+    const void* B;
+    const void* in0;
+    const void* in1;
+    void* out0;
+    void* out1;
+    double alpha, beta;
+    void* ws;
+    size_t ws_bytes;
+    mep_stream_t stream;
+    void* flush_buf;
+    size_t flush_bytes;
+} mep_call_t;
+
+/* Runs one call as described above (the same checks, the same kernels). */
+int mep_run(const mep_call_t* call);
+
+/*
+ * Trimmed-mean timing of Eq. 3 (Sec. 3.2): `warmup` untimed calls, then R
+ * samples; sample r is the elapsed device time (HIP events on call->stream)
+ * of `inner` back-to-back calls divided by `inner`, preceded (outside the
+ * timed interval) by a cache flush when flush != 0 and call->flush_buf is
+ * set.  The samples are sorted, the k lowest and k highest dropped and the
+ * remaining R - 2k averaged into *mean_ms.  samples_ms (nullable) receives
+ * the R samples in run order.  Requires R > 2k >= 0, inner >= 1, warmup >= 0
+ * (MEP_EBUDGET otherwise).  Synchronizes call->stream.  The paper uses R = 30,
+ * k = 3 (Sec. 4.1.3).
+ */
+int mep_time_trimmed(const mep_call_t* call, int warmup, int R, int k, int inner, int flush,
+                     double* mean_ms, double* samples_ms);
+
+/*
+ * Eq. 3 on host samples: mean of the sorted samples with the k lowest and k
+ * highest removed, summed in ascending order.  NaN if R <= 2k or k < 0.
+ */
+double mep_trimmed_mean(const double* samples, int R, int k);
+
+/*
+ * Functional-equivalence check (Eq. 4, "output consistency"): compares the
+ * host copy `out` (len elements of dtype) with a host fp64 reference.
+ * *err = max_i |out_i - ref_i| / max_i |ref_i| (normwise relative error);
+ * +inf if any out_i is not finite, or if ref is all zero and out is not.
+ * *pass = (*err <= tol).  len = 0 passes with *err = 0.
+ */
+int mep_check_fe(int dtype, const void* out, const double* ref, int64_t len, double tol,
+                 double* err, int* pass);
+
+/*
+ * Kernel candidates (Sec. 3.2, Eqs. 4-5).  The paper's loop ranks N candidate
+ * kernels per round by trimmed-mean time among those that pass FE.  Here the
+ * candidates are the library's own hand-written kernel shapes for an
+ * operation: mep_variant_count() gives how many there are for an op, dtype
+ * and shape (>= 1; 0 on bad arguments), and mep_set_variant(op, v) makes
+ * every later call of op use candidate v (-1 restores the default, candidate
+ * 0; a v beyond the count of a later shape also means the default).
+ * mep_workspace_bytes() already covers every candidate.  The setting is
+ * process-wide; it changes speed only, never the checks or the contract.
+ */
+int mep_variant_count(int op, int dtype, int64_t m, int64_t n);
+int mep_set_variant(int op, int variant);
+
+/*
+ * Device-time instrumentation of the dominant (matrix-streaming) kernel.
+ * mep_profile_begin(cap) arms up to cap records; while armed, every operation
+ * records a HIP event pair around its streaming kernel on its own stream.
+ * mep_profile_end() synchronizes those events, returns the number of
+ * recorded launches and their summed duration, and disarms.  Not thread-safe.
+ */
+int mep_profile_begin(int capacity);
+int mep_profile_end(double* total_ms, int* launches);
+
+/*
+ * Plain device copy of `bytes` bytes (16-byte vector loads and stores):
+ * the streaming ceiling probe used to calibrate memory-traffic counters and
+ * achievable bandwidth.  src and dst must be 16-byte aligned, must not
+ * overlap, and bytes must be a multiple of 16.
+ */
+int mep_stream_copy(const void* src, void* dst, size_t bytes, mep_stream_t stream);
+
+/* Description of the last error on the calling thread ("" if none). */
+const char* mep_last_error(void);
+
+/* Library version string. */
+const char* mep_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MEP_H */

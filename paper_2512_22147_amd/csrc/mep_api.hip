@@ -1,0 +1,855 @@
+// C-ABI of libmep.so (include/mep.h): argument checks, planning, launch
+// sequences of the matrix-vector operations and the minimal-executable-
+// program harness (trimmed-mean timing of Eq. 3, functional-equivalence
+// check of Eq. 4, candidate selection for Eqs. 4-5).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <atomic>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <limits>
+#include <string>
+#include <vector>
+
+#include "mep.h"
+#include "mep_internal.hpp"
+
+namespace mep {
+
+// ---------------------------------------------------------------------------
+// errors
+// ---------------------------------------------------------------------------
+
+static thread_local std::string g_last_error;
+
+static int fail(int code, const char* fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return code;
+}
+
+static int hip_fail(hipError_t e, const char* what)
+{
+    return fail(MEP_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// ---------------------------------------------------------------------------
+// planning
+// ---------------------------------------------------------------------------
+
+constexpr int64_t kMaxDim = int64_t(1) << 30;
+constexpr int64_t kMaxRow = int64_t(65535) * 8192;
+
+static int esize_of(int dtype) { return dtype == MEP_F32 ? 4 : (dtype == MEP_F64 ? 8 : 0); }
+
+int stream_candidates(int esize, bool vec, int mode, int64_t n, int* idx)
+{
+    const int vw = vec ? 16 / esize : 1;
+    const int vgpr32 = vec ? 4 : esize / 4;
+    const Cfg* tab = vec ? kVecCfg : kScalarCfg;
+    const int nt = vec ? kNumVecCfg : kNumScalarCfg;
+    const int64_t nv = (n + vw - 1) / vw;
+    int cnt = 0;
+    int64_t first_cap = -1;
+    // shapes that hold a whole row, narrowest first; much wider ones only idle lanes
+    for (int i = 0; i < nt && cnt < 16; ++i) {
+        const Cfg c = tab[i];
+        const int64_t cap = (int64_t)c.G * c.V;
+        if (!cfg_fits(c, mode, vgpr32) || cap < nv)
+            continue;
+        if (first_cap < 0)
+            first_cap = cap;
+        if (cap > 4 * first_cap)
+            continue;
+        idx[cnt++] = i;
+    }
+    if (cnt == 0) {
+        // rows longer than any shape: the widest shapes, over column panels
+        int64_t best = 0;
+        for (int i = 0; i < nt; ++i)
+            if (cfg_fits(tab[i], mode, vgpr32) && tab[i].G >= 64)
+                best = std::max<int64_t>(best, (int64_t)tab[i].G * tab[i].V);
+        for (int i = 0; i < nt && cnt < 16; ++i)
+            if (cfg_fits(tab[i], mode, vgpr32) && tab[i].G >= 64 &&
+                (int64_t)tab[i].G * tab[i].V == best)
+                idx[cnt++] = i;
+    }
+    return cnt;
+}
+
+Plan plan_stream(int esize, bool vec, int mode, int64_t m, int64_t n, int variant)
+{
+    int idx[16];
+    const int cnt = stream_candidates(esize, vec, mode, n, idx);
+    const int k = (variant >= 0 && variant < cnt) ? variant : 0;
+    Plan p;
+    p.vec = vec;
+    p.vw = vec ? 16 / esize : 1;
+    p.cfg = idx[k];
+    p.c = vec ? kVecCfg[p.cfg] : kScalarCfg[p.cfg];
+    p.threads = p.c.G < 256 ? 256 : p.c.G;
+    p.pw = (int64_t)p.c.G * p.c.V * p.vw;
+    p.panels = std::max<int64_t>(1, (n + p.pw - 1) / p.pw);
+    const int64_t rows_per_block = (int64_t)batch_of(p.c.B, mode) * (p.threads / p.c.G);
+    const int64_t nblk = (m + rows_per_block - 1) / rows_per_block;
+    // enough workgroups to fill the 256 compute units at the shape's occupancy
+    const int64_t per_cu = p.threads <= 256 ? 4 : (p.threads == 512 && p.c.WPE >= 4 ? 2 : 1);
+    p.nb = std::max<int64_t>(1, std::min<int64_t>(nblk, 256 * per_cu));
+    return p;
+}
+
+static std::atomic<int> g_variant[5] = {{-1}, {-1}, {-1}, {-1}, {-1}};
+
+static int op_mode(int op)
+{
+    switch (op) {
+    case MEP_OP_MATVEC: return MODE_MV;
+    case MEP_OP_MATVEC_T: return MODE_ATW;
+    case MEP_OP_BICG: return MODE_BICG;
+    case MEP_OP_ATA_X: return MODE_ATAX;
+    case MEP_OP_AXPBY_MV: return MODE_AXPBY;
+    default: return -1;
+    }
+}
+
+static size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
+
+// Workspace pieces of one plan: column partials (nb rows of n), partial dots
+// of column panels (panels rows of m, twice for two matrices) and, for the
+// two-pass ATAX, the intermediate t.
+struct WsLayout {
+    size_t colpart, dotpart, dotpart2, tvec, total;
+};
+
+static WsLayout layout_for(int mode, const Plan& p, int esize, int64_t m, int64_t n, bool need_t)
+{
+    WsLayout w{0, 0, 0, 0, 0};
+    if (mode & F_COL)
+        w.colpart = align256((size_t)p.nb * (size_t)n * esize);
+    if ((mode & F_DOT) && p.panels > 1) {
+        w.dotpart = align256((size_t)p.panels * (size_t)m * esize);
+        if (mode & F_TWO)
+            w.dotpart2 = w.dotpart;
+    }
+    if (need_t)
+        w.tvec = align256((size_t)m * esize);
+    w.total = w.colpart + w.dotpart + w.dotpart2 + w.tvec;
+    return w;
+}
+
+static bool vec_ok_n(int esize, int64_t n) { return n % (16 / esize) == 0; }
+static bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+// Largest workspace over both load paths and every candidate shape.
+static size_t ws_bytes_mode(int mode, int esize, int64_t m, int64_t n)
+{
+    if (m == 0 || n == 0)
+        return 0;
+    size_t best = 0;
+    for (int v = 0; v < 2; ++v) {
+        const bool vec = v == 0;
+        if (vec && !vec_ok_n(esize, n))
+            continue;
+        int idx[16];
+        const int cnt = stream_candidates(esize, vec, mode, n, idx);
+        for (int k = 0; k < cnt; ++k) {
+            const Plan p = plan_stream(esize, vec, mode, m, n, k);
+            if (mode == MODE_ATAX && p.panels > 1) {
+                // two passes: A x over panels, then A^T t over panels
+                size_t s = 0;
+                for (int k2 = 0; k2 < 16; ++k2) {
+                    int i1[16], i2[16];
+                    const int c1 = stream_candidates(esize, vec, MODE_MV, n, i1);
+                    const int c2 = stream_candidates(esize, vec, MODE_ATW, n, i2);
+                    if (k2 >= c1 && k2 >= c2)
+                        break;
+                    const Plan p1 = plan_stream(esize, vec, MODE_MV, m, n, k2 < c1 ? k2 : 0);
+                    const Plan p2 = plan_stream(esize, vec, MODE_ATW, m, n, k2 < c2 ? k2 : 0);
+                    const WsLayout l1 = layout_for(MODE_MV, p1, esize, m, n, true);
+                    const WsLayout l2 = layout_for(MODE_ATW, p2, esize, m, n, false);
+                    s = std::max(s, l1.dotpart + l1.tvec + l2.colpart);
+                }
+                best = std::max(best, s);
+            } else {
+                best = std::max(best, layout_for(mode, p, esize, m, n, false).total);
+            }
+        }
+    }
+    return best;
+}
+
+// ---------------------------------------------------------------------------
+// argument checks (pure host code: nothing here touches the GPU)
+// ---------------------------------------------------------------------------
+
+struct Range {
+    const void* p;
+    size_t bytes;
+    const char* name;
+};
+
+static int check_sizes(int dtype, int64_t m, int64_t n)
+{
+    if (esize_of(dtype) == 0)
+        return fail(MEP_EINVAL, "dtype %d is neither MEP_F32 nor MEP_F64", dtype);
+    if (m < 0 || n < 0)
+        return fail(MEP_EINVAL, "negative size m=%lld n=%lld", (long long)m, (long long)n);
+    if (m > kMaxDim || n > kMaxDim)
+        return fail(MEP_EINVAL, "size above 2^30: m=%lld n=%lld", (long long)m, (long long)n);
+    // rows are cut into at most 65535 column panels of >= 8192 elements
+    if (n > kMaxRow)
+        return fail(MEP_EINVAL, "row length n=%lld above %lld", (long long)n, (long long)kMaxRow);
+    return MEP_OK;
+}
+
+static int check_ptr(const void* p, int64_t count, int esize, const char* name)
+{
+    if (count > 0 && p == nullptr)
+        return fail(MEP_EINVAL, "%s is NULL but has %lld elements", name, (long long)count);
+    if (p != nullptr && !aligned(p, (size_t)esize))
+        return fail(MEP_EALIGN, "%s is not aligned to %d bytes", name, esize);
+    return MEP_OK;
+}
+
+static bool overlap(const Range& a, const Range& b)
+{
+    if (a.p == nullptr || b.p == nullptr || a.bytes == 0 || b.bytes == 0)
+        return false;
+    const uintptr_t a0 = (uintptr_t)a.p, a1 = a0 + a.bytes;
+    const uintptr_t b0 = (uintptr_t)b.p, b1 = b0 + b.bytes;
+    return a0 < b1 && b0 < a1;
+}
+
+// outputs must not overlap any other range (inputs, workspace, other outputs)
+static int check_overlaps(const Range* outs, int nout, const Range* ins, int nin)
+{
+    for (int i = 0; i < nout; ++i) {
+        for (int j = 0; j < nin; ++j)
+            if (overlap(outs[i], ins[j]))
+                return fail(MEP_EINVAL, "output %s overlaps %s", outs[i].name, ins[j].name);
+        for (int j = i + 1; j < nout; ++j)
+            if (overlap(outs[i], outs[j]))
+                return fail(MEP_EINVAL, "outputs %s and %s overlap", outs[i].name, outs[j].name);
+    }
+    return MEP_OK;
+}
+
+static int check_ws(void* ws, size_t ws_bytes, size_t need)
+{
+    if (need == 0)
+        return MEP_OK;
+    if (ws == nullptr || ws_bytes < need)
+        return fail(MEP_EWORKSPACE, "workspace of %zu bytes given, %zu needed", ws == nullptr ? 0 : ws_bytes,
+                    need);
+    if (!aligned(ws, 256))
+        return fail(MEP_EALIGN, "workspace is not aligned to 256 bytes");
+    return MEP_OK;
+}
+
+// ---------------------------------------------------------------------------
+// profiling of the streaming kernel
+// ---------------------------------------------------------------------------
+
+struct Prof {
+    bool armed = false;
+    int cap = 0, used = 0;
+    std::vector<hipEvent_t> start, stop;
+};
+static Prof g_prof;
+
+static void prof_begin_mark(hipStream_t s)
+{
+    if (g_prof.armed && g_prof.used < g_prof.cap)
+        (void)hipEventRecord(g_prof.start[g_prof.used], s);
+}
+
+static void prof_end_mark(hipStream_t s)
+{
+    if (g_prof.armed && g_prof.used < g_prof.cap) {
+        (void)hipEventRecord(g_prof.stop[g_prof.used], s);
+        ++g_prof.used;
+    }
+}
+
+template <typename T>
+static hipError_t stream_launch(const Plan& p, int mode, const StreamArgs<T>& a, hipStream_t s)
+{
+    if (p.panels > 65535 || p.nb > 65535)
+        return hipErrorInvalidConfiguration;  // beyond the grid limits; sizes are checked first
+    prof_begin_mark(s);
+    const hipError_t e = launch_stream<T>(p, mode, a, s);
+    prof_end_mark(s);
+    return e;
+}
+
+static int variant_of(int op) { return g_variant[op].load(std::memory_order_relaxed); }
+
+// ---------------------------------------------------------------------------
+// operations
+// ---------------------------------------------------------------------------
+
+template <typename T>
+static StreamArgs<T> empty_args(int64_t m, int64_t n)
+{
+    StreamArgs<T> a;
+    std::memset(&a, 0, sizeof a);
+    a.m = m;
+    a.n = n;
+    a.ldp = n;
+    return a;
+}
+
+template <typename T>
+static int run_matvec(int64_t m, int64_t n, const T* A, const T* x, T* y, char* ws, hipStream_t s)
+{
+    hipError_t e = hipSuccess;
+    if (m == 0)
+        return MEP_OK;
+    if (n == 0) {
+        e = launch_fill_zero<T>(y, m, s);
+        return e == hipSuccess ? MEP_OK : hip_fail(e, "fill");
+    }
+    const bool vec = vec_ok_n(sizeof(T), n) && aligned(A, 16) && aligned(x, 16);
+    const Plan p = plan_stream(sizeof(T), vec, MODE_MV, m, n, variant_of(MEP_OP_MATVEC));
+    StreamArgs<T> a = empty_args<T>(m, n);
+    a.A = A;
+    a.x = x;
+    if (p.panels == 1) {
+        a.rowout = y;
+        e = stream_launch<T>(p, MODE_MV, a, s);
+    } else {
+        a.dotpart = reinterpret_cast<T*>(ws);
+        e = stream_launch<T>(p, MODE_MV, a, s);
+        if (e == hipSuccess)
+            e = launch_colreduce<T>(a.dotpart, nullptr, m, p.panels, m, (T)1, (T)0, y, s);
+    }
+    return e == hipSuccess ? MEP_OK : hip_fail(e, "matvec launch");
+}
+
+template <typename T>
+static int run_matvec_t(int64_t m, int64_t n, const T* A, const T* w, T* z, const T* pv, T* q, bool pair,
+                        char* ws, hipStream_t s)
+{
+    hipError_t e = hipSuccess;
+    if (n == 0) {
+        if (pair && m > 0)
+            e = launch_fill_zero<T>(q, m, s);
+        return e == hipSuccess ? MEP_OK : hip_fail(e, "fill");
+    }
+    if (m == 0) {
+        e = launch_fill_zero<T>(z, n, s);
+        return e == hipSuccess ? MEP_OK : hip_fail(e, "fill");
+    }
+    const int mode = pair ? MODE_BICG : MODE_ATW;
+    const int op = pair ? MEP_OP_BICG : MEP_OP_MATVEC_T;
+    const bool vec = vec_ok_n(sizeof(T), n) && aligned(A, 16) && (!pair || aligned(pv, 16));
+    const Plan p = plan_stream(sizeof(T), vec, mode, m, n, variant_of(op));
+    const WsLayout l = layout_for(mode, p, sizeof(T), m, n, false);
+    StreamArgs<T> a = empty_args<T>(m, n);
+    a.A = A;
+    a.x = pv;
+    a.w = w;
+    a.colpart = reinterpret_cast<T*>(ws);
+    if (pair) {
+        if (p.panels == 1)
+            a.rowout = q;
+        else
+            a.dotpart = reinterpret_cast<T*>(ws + l.colpart);
+    }
+    e = stream_launch<T>(p, mode, a, s);
+    if (e == hipSuccess)
+        e = launch_colreduce<T>(a.colpart, nullptr, n, p.nb, n, (T)1, (T)0, z, s);
+    if (e == hipSuccess && pair && p.panels > 1)
+        e = launch_colreduce<T>(a.dotpart, nullptr, m, p.panels, m, (T)1, (T)0, q, s);
+    return e == hipSuccess ? MEP_OK : hip_fail(e, "matvec_t launch");
+}
+
+template <typename T>
+static int run_ata_x(int64_t m, int64_t n, const T* A, const T* x, T* y, T* t, char* ws, hipStream_t s)
+{
+    hipError_t e = hipSuccess;
+    if (n == 0) {
+        if (t != nullptr && m > 0)
+            e = launch_fill_zero<T>(t, m, s);
+        return e == hipSuccess ? MEP_OK : hip_fail(e, "fill");
+    }
+    if (m == 0) {
+        e = launch_fill_zero<T>(y, n, s);
+        return e == hipSuccess ? MEP_OK : hip_fail(e, "fill");
+    }
+    const bool vec = vec_ok_n(sizeof(T), n) && aligned(A, 16) && aligned(x, 16);
+    const Plan p = plan_stream(sizeof(T), vec, MODE_ATAX, m, n, variant_of(MEP_OP_ATA_X));
+    if (p.panels == 1) {
+        // one pass: row dot, then the same row scaled by it into the column sums
+        StreamArgs<T> a = empty_args<T>(m, n);
+        a.A = A;
+        a.x = x;
+        a.rowout = t;
+        a.colpart = reinterpret_cast<T*>(ws);
+        e = stream_launch<T>(p, MODE_ATAX, a, s);
+        if (e == hipSuccess)
+            e = launch_colreduce<T>(a.colpart, nullptr, n, p.nb, n, (T)1, (T)0, y, s);
+        return e == hipSuccess ? MEP_OK : hip_fail(e, "ata_x launch");
+    }
+    // rows too long to keep on chip: t = A x over column panels, then A^T t
+    const Plan p1 = plan_stream(sizeof(T), vec, MODE_MV, m, n, variant_of(MEP_OP_ATA_X));
+    const Plan p2 = plan_stream(sizeof(T), vec, MODE_ATW, m, n, variant_of(MEP_OP_ATA_X));
+    const WsLayout l1 = layout_for(MODE_MV, p1, sizeof(T), m, n, true);
+    T* dot = reinterpret_cast<T*>(ws);
+    T* tt = t != nullptr ? t : reinterpret_cast<T*>(ws + l1.dotpart);
+    T* colpart = reinterpret_cast<T*>(ws + l1.dotpart + l1.tvec);
+    StreamArgs<T> a1 = empty_args<T>(m, n);
+    a1.A = A;
+    a1.x = x;
+    a1.dotpart = dot;
+    if (p1.panels == 1)
+        a1.rowout = tt;
+    e = stream_launch<T>(p1, MODE_MV, a1, s);
+    if (e == hipSuccess && p1.panels > 1)
+        e = launch_colreduce<T>(dot, nullptr, m, p1.panels, m, (T)1, (T)0, tt, s);
+    if (e == hipSuccess) {
+        StreamArgs<T> a2 = empty_args<T>(m, n);
+        a2.A = A;
+        a2.w = tt;
+        a2.colpart = colpart;
+        e = stream_launch<T>(p2, MODE_ATW, a2, s);
+        if (e == hipSuccess)
+            e = launch_colreduce<T>(colpart, nullptr, n, p2.nb, n, (T)1, (T)0, y, s);
+    }
+    return e == hipSuccess ? MEP_OK : hip_fail(e, "ata_x launch");
+}
+
+template <typename T>
+static int run_axpby(int64_t m, int64_t n, T alpha, const T* A, T beta, const T* B, const T* x, T* y,
+                     char* ws, hipStream_t s)
+{
+    hipError_t e = hipSuccess;
+    if (m == 0)
+        return MEP_OK;
+    if (n == 0) {
+        e = launch_fill_zero<T>(y, m, s);
+        return e == hipSuccess ? MEP_OK : hip_fail(e, "fill");
+    }
+    const bool vec = vec_ok_n(sizeof(T), n) && aligned(A, 16) && aligned(B, 16) && aligned(x, 16);
+    const Plan p = plan_stream(sizeof(T), vec, MODE_AXPBY, m, n, variant_of(MEP_OP_AXPBY_MV));
+    const WsLayout l = layout_for(MODE_AXPBY, p, sizeof(T), m, n, false);
+    StreamArgs<T> a = empty_args<T>(m, n);
+    a.A = A;
+    a.B = B;
+    a.x = x;
+    a.alpha = alpha;
+    a.beta = beta;
+    if (p.panels == 1) {
+        a.rowout = y;
+        e = stream_launch<T>(p, MODE_AXPBY, a, s);
+    } else {
+        a.dotpart = reinterpret_cast<T*>(ws);
+        a.dotpart2 = reinterpret_cast<T*>(ws + l.dotpart);
+        e = stream_launch<T>(p, MODE_AXPBY, a, s);
+        if (e == hipSuccess)
+            e = launch_colreduce<T>(a.dotpart, a.dotpart2, m, p.panels, m, alpha, beta, y, s);
+    }
+    return e == hipSuccess ? MEP_OK : hip_fail(e, "axpby_mv launch");
+}
+
+// ---------------------------------------------------------------------------
+// streaming copy (ceiling probe) and cache flush
+// ---------------------------------------------------------------------------
+
+constexpr int kCopyUnroll = 4;
+
+__global__ void __launch_bounds__(256) k_copy16(const uint4* __restrict__ src, uint4* __restrict__ dst,
+                                                int64_t count)
+{
+    const int64_t stride = (int64_t)gridDim.x * 256;
+    int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    for (; i + (kCopyUnroll - 1) * stride < count; i += kCopyUnroll * stride) {
+        uint4 v[kCopyUnroll];
+#pragma unroll
+        for (int u = 0; u < kCopyUnroll; ++u)
+            v[u] = src[i + u * stride];
+#pragma unroll
+        for (int u = 0; u < kCopyUnroll; ++u)
+            dst[i + u * stride] = v[u];
+    }
+    for (; i < count; i += stride)
+        dst[i] = src[i];
+}
+
+__global__ void __launch_bounds__(256) k_flush16(uint4* __restrict__ dst, int64_t count, uint32_t tag)
+{
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < count; i += (int64_t)gridDim.x * 256)
+        dst[i] = make_uint4(tag, (uint32_t)i, (uint32_t)(i >> 32), tag ^ 0xFFFFFFFFu);
+}
+
+hipError_t launch_copy16(const void* src, void* dst, size_t bytes, hipStream_t s)
+{
+    const int64_t count = (int64_t)(bytes / 16);
+    const int64_t blocks = std::min<int64_t>((count + 255) / 256, 256 * 16);
+    hipLaunchKernelGGL(k_copy16, dim3((unsigned)blocks), dim3(256), 0, s, (const uint4*)src, (uint4*)dst,
+                       count);
+    return hipGetLastError();
+}
+
+hipError_t launch_flush(void* buf, size_t bytes, uint32_t tag, hipStream_t s)
+{
+    const int64_t count = (int64_t)(bytes / 16);
+    if (count == 0)
+        return hipSuccess;
+    const int64_t blocks = std::min<int64_t>((count + 255) / 256, 256 * 16);
+    hipLaunchKernelGGL(k_flush16, dim3((unsigned)blocks), dim3(256), 0, s, (uint4*)buf, count, tag);
+    return hipGetLastError();
+}
+
+}  // namespace mep
+
+using namespace mep;
+
+// ---------------------------------------------------------------------------
+// extern "C" entry points
+// ---------------------------------------------------------------------------
+
+extern "C" {
+
+const char* mep_last_error(void) { return g_last_error.c_str(); }
+
+const char* mep_version(void) { return "mep 0.1 (gfx950)"; }
+
+size_t mep_workspace_bytes(int op, int dtype, int64_t m, int64_t n)
+{
+    const int es = esize_of(dtype);
+    const int mode = op_mode(op);
+    if (es == 0 || mode < 0 || m < 0 || n < 0 || m > kMaxDim || n > kMaxDim)
+        return 0;
+    return ws_bytes_mode(mode, es, m, n);
+}
+
+int mep_variant_count(int op, int dtype, int64_t m, int64_t n)
+{
+    const int es = esize_of(dtype);
+    const int mode = op_mode(op);
+    if (es == 0 || mode < 0 || m < 0 || n < 0 || m > kMaxDim || n > kMaxDim)
+        return 0;
+    int idx[16];
+    const bool vec = vec_ok_n(es, n);
+    return std::max(1, stream_candidates(es, vec, mode, std::max<int64_t>(n, 1), idx));
+}
+
+int mep_set_variant(int op, int variant)
+{
+    if (op_mode(op) < 0)
+        return fail(MEP_EINVAL, "unknown op %d", op);
+    g_variant[op].store(variant < 0 ? -1 : variant, std::memory_order_relaxed);
+    return MEP_OK;
+}
+
+int mep_matvec(int dtype, int64_t m, int64_t n, const void* A, const void* x, void* y, void* ws,
+               size_t ws_bytes, mep_stream_t stream)
+{
+    int rc = check_sizes(dtype, m, n);
+    if (rc)
+        return rc;
+    const int es = esize_of(dtype);
+    if ((rc = check_ptr(A, m * n, es, "A")) || (rc = check_ptr(x, n, es, "x")) ||
+        (rc = check_ptr(y, m, es, "y")))
+        return rc;
+    const size_t need = mep_workspace_bytes(MEP_OP_MATVEC, dtype, m, n);
+    if ((rc = check_ws(ws, ws_bytes, need)))
+        return rc;
+    const Range outs[] = {{y, (size_t)m * es, "y"}};
+    const Range ins[] = {{A, (size_t)(m * n) * es, "A"}, {x, (size_t)n * es, "x"}, {ws, need, "ws"}};
+    if ((rc = check_overlaps(outs, 1, ins, 3)))
+        return rc;
+    hipStream_t s = (hipStream_t)stream;
+    if (dtype == MEP_F32)
+        return run_matvec<float>(m, n, (const float*)A, (const float*)x, (float*)y, (char*)ws, s);
+    return run_matvec<double>(m, n, (const double*)A, (const double*)x, (double*)y, (char*)ws, s);
+}
+
+int mep_matvec_t(int dtype, int64_t m, int64_t n, const void* A, const void* w, void* z, const void* p,
+                 void* q, void* ws, size_t ws_bytes, mep_stream_t stream)
+{
+    int rc = check_sizes(dtype, m, n);
+    if (rc)
+        return rc;
+    // the pair is requested by either pointer; each may be NULL only when empty
+    const bool pair = p != nullptr || q != nullptr;
+    if (pair && ((p == nullptr && n > 0) || (q == nullptr && m > 0)))
+        return fail(MEP_EINVAL, "p and q must both be set for the paired product");
+    const int es = esize_of(dtype);
+    if ((rc = check_ptr(A, m * n, es, "A")) || (rc = check_ptr(w, m, es, "w")) ||
+        (rc = check_ptr(z, n, es, "z")))
+        return rc;
+    if (pair && ((rc = check_ptr(p, n, es, "p")) || (rc = check_ptr(q, m, es, "q"))))
+        return rc;
+    const size_t need = mep_workspace_bytes(pair ? MEP_OP_BICG : MEP_OP_MATVEC_T, dtype, m, n);
+    if ((rc = check_ws(ws, ws_bytes, need)))
+        return rc;
+    const Range outs[] = {{z, (size_t)n * es, "z"}, {q, pair ? (size_t)m * es : 0, "q"}};
+    const Range ins[] = {{A, (size_t)(m * n) * es, "A"},
+                         {w, (size_t)m * es, "w"},
+                         {p, pair ? (size_t)n * es : 0, "p"},
+                         {ws, need, "ws"}};
+    if ((rc = check_overlaps(outs, 2, ins, 4)))
+        return rc;
+    hipStream_t s = (hipStream_t)stream;
+    if (dtype == MEP_F32)
+        return run_matvec_t<float>(m, n, (const float*)A, (const float*)w, (float*)z, (const float*)p,
+                                   (float*)q, pair, (char*)ws, s);
+    return run_matvec_t<double>(m, n, (const double*)A, (const double*)w, (double*)z, (const double*)p,
+                                (double*)q, pair, (char*)ws, s);
+}
+
+int mep_ata_x(int dtype, int64_t m, int64_t n, const void* A, const void* x, void* y, void* t, void* ws,
+              size_t ws_bytes, mep_stream_t stream)
+{
+    int rc = check_sizes(dtype, m, n);
+    if (rc)
+        return rc;
+    const int es = esize_of(dtype);
+    if ((rc = check_ptr(A, m * n, es, "A")) || (rc = check_ptr(x, n, es, "x")) ||
+        (rc = check_ptr(y, n, es, "y")))
+        return rc;
+    if (t != nullptr && (rc = check_ptr(t, m, es, "t")))
+        return rc;
+    const size_t need = mep_workspace_bytes(MEP_OP_ATA_X, dtype, m, n);
+    if ((rc = check_ws(ws, ws_bytes, need)))
+        return rc;
+    const Range outs[] = {{y, (size_t)n * es, "y"}, {t, t ? (size_t)m * es : 0, "t"}};
+    const Range ins[] = {{A, (size_t)(m * n) * es, "A"}, {x, (size_t)n * es, "x"}, {ws, need, "ws"}};
+    if ((rc = check_overlaps(outs, 2, ins, 3)))
+        return rc;
+    hipStream_t s = (hipStream_t)stream;
+    if (dtype == MEP_F32)
+        return run_ata_x<float>(m, n, (const float*)A, (const float*)x, (float*)y, (float*)t, (char*)ws, s);
+    return run_ata_x<double>(m, n, (const double*)A, (const double*)x, (double*)y, (double*)t, (char*)ws, s);
+}
+
+int mep_axpby_mv(int dtype, int64_t m, int64_t n, double alpha, const void* A, double beta, const void* B,
+                 const void* x, void* y, void* ws, size_t ws_bytes, mep_stream_t stream)
+{
+    int rc = check_sizes(dtype, m, n);
+    if (rc)
+        return rc;
+    const int es = esize_of(dtype);
+    if ((rc = check_ptr(A, m * n, es, "A")) || (rc = check_ptr(B, m * n, es, "B")) ||
+        (rc = check_ptr(x, n, es, "x")) || (rc = check_ptr(y, m, es, "y")))
+        return rc;
+    const size_t need = mep_workspace_bytes(MEP_OP_AXPBY_MV, dtype, m, n);
+    if ((rc = check_ws(ws, ws_bytes, need)))
+        return rc;
+    const Range outs[] = {{y, (size_t)m * es, "y"}};
+    const Range ins[] = {{A, (size_t)(m * n) * es, "A"},
+                         {B, (size_t)(m * n) * es, "B"},
+                         {x, (size_t)n * es, "x"},
+                         {ws, need, "ws"}};
+    if ((rc = check_overlaps(outs, 1, ins, 4)))
+        return rc;
+    hipStream_t s = (hipStream_t)stream;
+    if (dtype == MEP_F32)
+        return run_axpby<float>(m, n, (float)alpha, (const float*)A, (float)beta, (const float*)B,
+                                (const float*)x, (float*)y, (char*)ws, s);
+    return run_axpby<double>(m, n, alpha, (const double*)A, beta, (const double*)B, (const double*)x,
+                             (double*)y, (char*)ws, s);
+}
+
+int mep_run(const mep_call_t* c)
+{
+    if (c == nullptr)
+        return fail(MEP_EINVAL, "call is NULL");
+    switch (c->op) {
+    case MEP_OP_MATVEC:
+        return mep_matvec(c->dtype, c->m, c->n, c->A, c->in0, c->out0, c->ws, c->ws_bytes, c->stream);
+    case MEP_OP_MATVEC_T:
+        return mep_matvec_t(c->dtype, c->m, c->n, c->A, c->in0, c->out0, nullptr, nullptr, c->ws,
+                            c->ws_bytes, c->stream);
+    case MEP_OP_BICG:
+        if ((c->in1 == nullptr && c->n > 0) || (c->out1 == nullptr && c->m > 0))
+            return fail(MEP_EINVAL, "BICG needs in1 = p and out1 = q");
+        return mep_matvec_t(c->dtype, c->m, c->n, c->A, c->in0, c->out0, c->in1, c->out1, c->ws,
+                            c->ws_bytes, c->stream);
+    case MEP_OP_ATA_X:
+        return mep_ata_x(c->dtype, c->m, c->n, c->A, c->in0, c->out0, c->out1, c->ws, c->ws_bytes,
+                         c->stream);
+    case MEP_OP_AXPBY_MV:
+        return mep_axpby_mv(c->dtype, c->m, c->n, c->alpha, c->A, c->beta, c->B, c->in0, c->out0, c->ws,
+                            c->ws_bytes, c->stream);
+    default:
+        return fail(MEP_EINVAL, "unknown op %d", c->op);
+    }
+}
+
+double mep_trimmed_mean(const double* samples, int R, int k)
+{
+    if (samples == nullptr || k < 0 || R <= 2 * k)
+        return std::numeric_limits<double>::quiet_NaN();
+    std::vector<double> v(samples, samples + R);
+    std::sort(v.begin(), v.end());
+    double sum = 0.0;
+    for (int i = k; i < R - k; ++i)
+        sum += v[i];
+    return sum / (double)(R - 2 * k);
+}
+
+int mep_time_trimmed(const mep_call_t* call, int warmup, int R, int k, int inner, int flush, double* mean_ms,
+                     double* samples_ms)
+{
+    if (call == nullptr || mean_ms == nullptr)
+        return fail(MEP_EINVAL, "call and mean_ms must be set");
+    if (k < 0 || R <= 2 * k)
+        return fail(MEP_EBUDGET, "Eq. 3 needs R > 2k >= 0 (R=%d, k=%d)", R, k);
+    if (inner < 1 || warmup < 0)
+        return fail(MEP_EBUDGET, "inner must be >= 1 and warmup >= 0");
+    if (flush && call->flush_buf != nullptr && (!aligned(call->flush_buf, 16) || call->flush_bytes % 16))
+        return fail(MEP_EALIGN, "flush buffer must be 16-byte aligned and a multiple of 16 bytes");
+    hipStream_t s = (hipStream_t)call->stream;
+    for (int i = 0; i < warmup; ++i) {
+        const int rc = mep_run(call);
+        if (rc)
+            return rc;
+    }
+    std::vector<hipEvent_t> ev(2 * (size_t)R, nullptr);
+    int rc = MEP_OK;
+    hipError_t e = hipSuccess;
+    for (size_t i = 0; i < ev.size() && e == hipSuccess; ++i)
+        e = hipEventCreate(&ev[i]);
+    for (int r = 0; r < R && e == hipSuccess && rc == MEP_OK; ++r) {
+        if (flush && call->flush_buf != nullptr && call->flush_bytes > 0)
+            e = launch_flush(call->flush_buf, call->flush_bytes, 0x9E3779B9u + (uint32_t)r, s);
+        if (e == hipSuccess)
+            e = hipEventRecord(ev[2 * r], s);
+        for (int i = 0; i < inner && e == hipSuccess && rc == MEP_OK; ++i)
+            rc = mep_run(call);
+        if (e == hipSuccess && rc == MEP_OK)
+            e = hipEventRecord(ev[2 * r + 1], s);
+    }
+    if (e == hipSuccess)
+        e = hipStreamSynchronize(s);
+    std::vector<double> samples((size_t)R, 0.0);
+    for (int r = 0; r < R && e == hipSuccess && rc == MEP_OK; ++r) {
+        float ms = 0.f;
+        e = hipEventElapsedTime(&ms, ev[2 * r], ev[2 * r + 1]);
+        samples[r] = (double)ms / inner;
+    }
+    for (hipEvent_t x : ev)
+        if (x != nullptr)
+            (void)hipEventDestroy(x);
+    if (rc)
+        return rc;
+    if (e != hipSuccess)
+        return hip_fail(e, "timing");
+    if (samples_ms != nullptr)
+        std::memcpy(samples_ms, samples.data(), sizeof(double) * R);
+    *mean_ms = mep_trimmed_mean(samples.data(), R, k);
+    return MEP_OK;
+}
+
+int mep_check_fe(int dtype, const void* out, const double* ref, int64_t len, double tol, double* err, int* pass)
+{
+    if (esize_of(dtype) == 0)
+        return fail(MEP_EINVAL, "dtype %d is neither MEP_F32 nor MEP_F64", dtype);
+    if (len < 0 || err == nullptr || pass == nullptr || (len > 0 && (out == nullptr || ref == nullptr)))
+        return fail(MEP_EINVAL, "bad arguments to mep_check_fe");
+    double worst = 0.0, scale = 0.0;
+    bool finite = true;
+    for (int64_t i = 0; i < len; ++i) {
+        const double o = dtype == MEP_F32 ? (double)((const float*)out)[i] : ((const double*)out)[i];
+        if (!std::isfinite(o))
+            finite = false;
+        scale = std::max(scale, std::fabs(ref[i]));
+        worst = std::max(worst, std::fabs(o - ref[i]));
+    }
+    double e;
+    if (!finite)
+        e = std::numeric_limits<double>::infinity();
+    else if (scale == 0.0)
+        e = worst == 0.0 ? 0.0 : std::numeric_limits<double>::infinity();
+    else
+        e = worst / scale;
+    *err = e;
+    *pass = e <= tol ? 1 : 0;
+    return MEP_OK;
+}
+
+int mep_profile_begin(int capacity)
+{
+    if (capacity < 1)
+        return fail(MEP_EINVAL, "capacity must be >= 1");
+    if (g_prof.armed)
+        return fail(MEP_EINVAL, "profiling is already armed");
+    g_prof.start.assign((size_t)capacity, nullptr);
+    g_prof.stop.assign((size_t)capacity, nullptr);
+    for (int i = 0; i < capacity; ++i) {
+        hipError_t e = hipEventCreate(&g_prof.start[i]);
+        if (e == hipSuccess)
+            e = hipEventCreate(&g_prof.stop[i]);
+        if (e != hipSuccess) {
+            for (hipEvent_t x : g_prof.start)
+                if (x)
+                    (void)hipEventDestroy(x);
+            for (hipEvent_t x : g_prof.stop)
+                if (x)
+                    (void)hipEventDestroy(x);
+            g_prof.start.clear();
+            g_prof.stop.clear();
+            return hip_fail(e, "event create");
+        }
+    }
+    g_prof.cap = capacity;
+    g_prof.used = 0;
+    g_prof.armed = true;
+    return MEP_OK;
+}
+
+int mep_profile_end(double* total_ms, int* launches)
+{
+    if (!g_prof.armed)
+        return fail(MEP_EINVAL, "profiling is not armed");
+    double tot = 0.0;
+    hipError_t e = hipSuccess;
+    for (int i = 0; i < g_prof.used && e == hipSuccess; ++i) {
+        e = hipEventSynchronize(g_prof.stop[i]);
+        float ms = 0.f;
+        if (e == hipSuccess)
+            e = hipEventElapsedTime(&ms, g_prof.start[i], g_prof.stop[i]);
+        tot += ms;
+    }
+    const int used = g_prof.used;
+    for (hipEvent_t x : g_prof.start)
+        (void)hipEventDestroy(x);
+    for (hipEvent_t x : g_prof.stop)
+        (void)hipEventDestroy(x);
+    g_prof = Prof();
+    if (e != hipSuccess)
+        return hip_fail(e, "profile events");
+    if (total_ms)
+        *total_ms = tot;
+    if (launches)
+        *launches = used;
+    return MEP_OK;
+}
+
+int mep_stream_copy(const void* src, void* dst, size_t bytes, mep_stream_t stream)
+{
+    if (bytes == 0)
+        return MEP_OK;
+    if (src == nullptr || dst == nullptr)
+        return fail(MEP_EINVAL, "NULL pointer");
+    if (!aligned(src, 16) || !aligned(dst, 16) || bytes % 16)
+        return fail(MEP_EALIGN, "copy needs 16-byte aligned pointers and a multiple of 16 bytes");
+    const Range a{dst, bytes, "dst"}, b{src, bytes, "src"};
+    if (overlap(a, b))
+        return fail(MEP_EINVAL, "src and dst overlap");
+    const hipError_t e = launch_copy16(src, dst, bytes, (hipStream_t)stream);
+    return e == hipSuccess ? MEP_OK : hip_fail(e, "copy launch");
+}
+
+}  // extern "C"

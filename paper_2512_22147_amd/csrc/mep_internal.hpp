@@ -1,0 +1,96 @@
+// Internal host-side interface between the C-ABI layer and the kernel
+// launch tables.  Not installed; the public interface is include/mep.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "mep_kernels.hpp"
+
+namespace mep {
+
+// Row-group geometry of one streaming-kernel instance: G lanes per row
+// group, V vectors per lane, B rows per batch, WPE waves per SIMD.
+struct Cfg {
+    int G, V, B, WPE;
+};
+
+// Vector path (16-byte loads), ordered by row capacity G * V; among equal
+// capacities the preferred shape comes first.
+constexpr int kNumVecCfg = 12;
+constexpr Cfg kVecCfg[kNumVecCfg] = {
+    {16, 1, 8, 4},   {64, 1, 8, 4},   {64, 2, 4, 4},  {64, 4, 2, 4},
+    {256, 2, 4, 4},  {256, 4, 2, 4},  {1024, 2, 4, 4}, {1024, 4, 2, 4},
+    {512, 8, 1, 2},  {512, 8, 2, 2},  {512, 16, 1, 2}, {1024, 8, 1, 4}};
+// Element-wise path (rows not 16-byte aligned): one element per load.
+constexpr int kNumScalarCfg = 3;
+constexpr Cfg kScalarCfg[kNumScalarCfg] = {{64, 4, 2, 4}, {256, 4, 2, 4}, {1024, 8, 1, 4}};
+
+// Rows per batch an instance really uses: two-matrix modes (GESUMMV) hold
+// twice the rows in registers, so they take half the batch.
+constexpr int batch_of(int B, int mode) { return (mode & F_TWO) ? (B > 1 ? B / 2 : 1) : B; }
+
+// Rough per-lane register need of an instance (vgpr32 = registers per
+// loaded vector): two row buffers, the column sums, the register copy of
+// the dot vector and some fixed overhead.  Instances above the budget of
+// their occupancy target are never built or chosen.
+constexpr int vgpr_estimate(Cfg c, int mode, int vgpr32)
+{
+    const int mats = (mode & F_TWO) ? 2 : 1;
+    const int bufs = 2 * mats * batch_of(c.B, mode) * c.V * vgpr32;
+    const int col = (mode & F_COL) ? c.V * vgpr32 : 0;
+    const int xbytes = c.V * vgpr32 * 4;
+    const bool xlds = (mode & F_DOT) && xbytes > (c.WPE <= 2 ? 128 : 64);
+    const int x = ((mode & F_DOT) && !xlds) ? c.V * vgpr32 : 0;
+    return bufs + col + x + 24;
+}
+constexpr bool cfg_fits(Cfg c, int mode, int vgpr32) { return vgpr_estimate(c, mode, vgpr32) <= 512 / c.WPE; }
+
+struct Plan {
+    bool vec;         // 16-byte vector path
+    int vw;           // elements per load
+    int cfg;          // index into kVecCfg / kScalarCfg
+    Cfg c;
+    int threads;      // workgroup size
+    int64_t pw;       // columns per panel
+    int64_t panels;   // column panels (gridDim.y)
+    int64_t nb;       // row workgroups (gridDim.x)
+};
+
+// Candidate configurations for a row of n elements (a pure function of its
+// arguments: no device query).  Returns the count; fills idx[] (capacity 16).
+int stream_candidates(int esize, bool vec, int mode, int64_t n, int* idx);
+// The plan of candidate `variant` (-1: the default, candidate 0).
+Plan plan_stream(int esize, bool vec, int mode, int64_t m, int64_t n, int variant);
+
+template <typename T>
+hipError_t launch_stream(const Plan& p, int mode, const StreamArgs<T>& a, hipStream_t s);
+
+template <typename T>
+hipError_t launch_colreduce(const T* P, const T* Q, int64_t ldp, int64_t nrows, int64_t ncols,
+                            T alpha, T beta, T* out, hipStream_t s);
+
+template <typename T>
+hipError_t launch_fill_zero(T* p, int64_t count, hipStream_t s);
+
+// The per-dtype launch tables (mep_launch_f32.hip, mep_launch_f64.hip).
+template <>
+hipError_t launch_stream<float>(const Plan&, int, const StreamArgs<float>&, hipStream_t);
+template <>
+hipError_t launch_stream<double>(const Plan&, int, const StreamArgs<double>&, hipStream_t);
+template <>
+hipError_t launch_colreduce<float>(const float*, const float*, int64_t, int64_t, int64_t, float, float,
+                                   float*, hipStream_t);
+template <>
+hipError_t launch_colreduce<double>(const double*, const double*, int64_t, int64_t, int64_t, double,
+                                    double, double*, hipStream_t);
+template <>
+hipError_t launch_fill_zero<float>(float*, int64_t, hipStream_t);
+template <>
+hipError_t launch_fill_zero<double>(double*, int64_t, hipStream_t);
+
+hipError_t launch_copy16(const void* src, void* dst, size_t bytes, hipStream_t s);
+hipError_t launch_flush(void* buf, size_t bytes, uint32_t tag, hipStream_t s);
+
+}  // namespace mep

@@ -1,0 +1,290 @@
+"""Python binding of libmep.so (include/mep.h): argument marshalling only.
+
+Every computation runs in the library's HIP kernels; PyTorch only provides
+device memory and the stream.  The functions keep the C names.  Loading
+fails loudly when ``libmep.so`` has not been built: there is no fallback.
+
+Tensors passed to the operations must be contiguous CUDA (HIP) tensors of
+dtype float32 or float64.  Outputs and the workspace are allocated with torch
+when not given.  Operations are asynchronous on ``stream`` (default: torch's
+current stream), like the C functions.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmep.so")
+
+MEP_F32, MEP_F64 = 0, 1
+MEP_OK, MEP_EINVAL, MEP_EALIGN, MEP_EWORKSPACE, MEP_EHIP, MEP_EBUDGET = range(6)
+MEP_OP_MATVEC, MEP_OP_MATVEC_T, MEP_OP_BICG, MEP_OP_ATA_X, MEP_OP_AXPBY_MV = range(5)
+ERROR_NAMES = {1: "MEP_EINVAL", 2: "MEP_EALIGN", 3: "MEP_EWORKSPACE", 4: "MEP_EHIP", 5: "MEP_EBUDGET"}
+
+# Names exported by libmep.so, in the order include/mep.h declares them.
+EXPORTS = (
+    "mep_workspace_bytes", "mep_matvec", "mep_matvec_t", "mep_ata_x", "mep_axpby_mv",
+    "mep_run", "mep_time_trimmed", "mep_trimmed_mean", "mep_check_fe",
+    "mep_variant_count", "mep_set_variant", "mep_profile_begin", "mep_profile_end",
+    "mep_stream_copy", "mep_last_error", "mep_version",
+)
+
+
+class MepError(RuntimeError):
+    def __init__(self, code: int, message: str):
+        super().__init__(f"{ERROR_NAMES.get(code, code)}: {message}")
+        self.code = code
+
+
+class MepCall(ctypes.Structure):
+    """mep_call_t."""
+    _fields_ = [
+        ("op", ctypes.c_int), ("dtype", ctypes.c_int),
+        ("m", ctypes.c_int64), ("n", ctypes.c_int64),
+        ("A", ctypes.c_void_p), ("B", ctypes.c_void_p),
+        ("in0", ctypes.c_void_p), ("in1", ctypes.c_void_p),
+        ("out0", ctypes.c_void_p), ("out1", ctypes.c_void_p),
+        ("alpha", ctypes.c_double), ("beta", ctypes.c_double),
+        ("ws", ctypes.c_void_p), ("ws_bytes", ctypes.c_size_t),
+        ("stream", ctypes.c_void_p),
+        ("flush_buf", ctypes.c_void_p), ("flush_bytes", ctypes.c_size_t),
+    ]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library with typed entry points."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                           "`python -m paper_2512_22147_amd.build` (no fallback exists)")
+    L = ctypes.CDLL(LIB_PATH)
+    i, i64, vp, d, sz = ctypes.c_int, ctypes.c_int64, ctypes.c_void_p, ctypes.c_double, ctypes.c_size_t
+    L.mep_workspace_bytes.argtypes = [i, i, i64, i64]
+    L.mep_workspace_bytes.restype = sz
+    L.mep_matvec.argtypes = [i, i64, i64, vp, vp, vp, vp, sz, vp]
+    L.mep_matvec_t.argtypes = [i, i64, i64, vp, vp, vp, vp, vp, vp, sz, vp]
+    L.mep_ata_x.argtypes = [i, i64, i64, vp, vp, vp, vp, vp, sz, vp]
+    L.mep_axpby_mv.argtypes = [i, i64, i64, d, vp, d, vp, vp, vp, vp, sz, vp]
+    L.mep_run.argtypes = [ctypes.POINTER(MepCall)]
+    L.mep_time_trimmed.argtypes = [ctypes.POINTER(MepCall), i, i, i, i, i,
+                                   ctypes.POINTER(d), ctypes.POINTER(d)]
+    L.mep_trimmed_mean.argtypes = [ctypes.POINTER(d), i, i]
+    L.mep_trimmed_mean.restype = d
+    L.mep_check_fe.argtypes = [i, vp, ctypes.POINTER(d), i64, d, ctypes.POINTER(d),
+                               ctypes.POINTER(ctypes.c_int)]
+    L.mep_variant_count.argtypes = [i, i, i64, i64]
+    L.mep_set_variant.argtypes = [i, i]
+    L.mep_profile_begin.argtypes = [i]
+    L.mep_profile_end.argtypes = [ctypes.POINTER(d), ctypes.POINTER(ctypes.c_int)]
+    L.mep_stream_copy.argtypes = [vp, vp, sz, vp]
+    L.mep_last_error.restype = ctypes.c_char_p
+    L.mep_version.restype = ctypes.c_char_p
+    _lib = L
+    return L
+
+
+def _check(rc: int) -> None:
+    if rc != MEP_OK:
+        raise MepError(rc, lib().mep_last_error().decode())
+
+
+def mep_last_error() -> str:
+    return lib().mep_last_error().decode()
+
+
+def mep_version() -> str:
+    return lib().mep_version().decode()
+
+
+# ---------------------------------------------------------------------------
+# torch marshalling
+# ---------------------------------------------------------------------------
+
+def _torch():
+    import torch
+
+    return torch
+
+
+def dtype_code(dtype) -> int:
+    torch = _torch()
+    if dtype == torch.float32:
+        return MEP_F32
+    if dtype == torch.float64:
+        return MEP_F64
+    raise TypeError(f"unsupported dtype {dtype}; use float32 or float64")
+
+
+def _ptr(t) -> int:
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("tensors must live on the GPU")
+    if not t.is_contiguous():
+        raise ValueError("tensors must be contiguous")
+    return t.data_ptr() if t.numel() > 0 else None
+
+
+def _stream(stream) -> int:
+    torch = _torch()
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream
+
+
+def _ws(op, A, ws):
+    torch = _torch()
+    m, n = A.shape
+    need = mep_workspace_bytes(op, dtype_code(A.dtype), m, n)
+    if ws is None and need > 0:
+        ws = torch.empty(need, dtype=torch.uint8, device=A.device)
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    return ws, nbytes
+
+
+def _out(like, n, out):
+    torch = _torch()
+    if out is None:
+        out = torch.empty(n, dtype=like.dtype, device=like.device)
+    return out
+
+
+def mep_workspace_bytes(op: int, dtype: int, m: int, n: int) -> int:
+    return int(lib().mep_workspace_bytes(op, dtype, m, n))
+
+
+def mep_matvec(A, x, y=None, ws=None, stream=None):
+    """y = A x."""
+    m, n = A.shape
+    y = _out(A, m, y)
+    ws, wsb = _ws(MEP_OP_MATVEC, A, ws)
+    _check(lib().mep_matvec(dtype_code(A.dtype), m, n, _ptr(A), _ptr(x), _ptr(y),
+                            _ptr(ws), wsb, _stream(stream)))
+    return y
+
+
+def mep_matvec_t(A, w, z=None, p=None, q=None, ws=None, stream=None):
+    """z = A^T w; with p, also q = A p in the same read of A (BICG)."""
+    m, n = A.shape
+    z = _out(A, n, z)
+    if p is not None and q is None:
+        q = _out(A, m, None)
+    ws, wsb = _ws(MEP_OP_BICG if p is not None else MEP_OP_MATVEC_T, A, ws)
+    _check(lib().mep_matvec_t(dtype_code(A.dtype), m, n, _ptr(A), _ptr(w), _ptr(z),
+                              _ptr(p), _ptr(q), _ptr(ws), wsb, _stream(stream)))
+    return (z, q) if p is not None else z
+
+
+def mep_ata_x(A, x, y=None, t=None, ws=None, stream=None):
+    """y = A^T (A x); t (optional) receives A x."""
+    m, n = A.shape
+    y = _out(A, n, y)
+    ws, wsb = _ws(MEP_OP_ATA_X, A, ws)
+    _check(lib().mep_ata_x(dtype_code(A.dtype), m, n, _ptr(A), _ptr(x), _ptr(y), _ptr(t),
+                           _ptr(ws), wsb, _stream(stream)))
+    return y
+
+
+def mep_axpby_mv(alpha, A, beta, B, x, y=None, ws=None, stream=None):
+    """y = alpha A x + beta B x."""
+    m, n = A.shape
+    y = _out(A, m, y)
+    ws, wsb = _ws(MEP_OP_AXPBY_MV, A, ws)
+    _check(lib().mep_axpby_mv(dtype_code(A.dtype), m, n, float(alpha), _ptr(A), float(beta),
+                              _ptr(B), _ptr(x), _ptr(y), _ptr(ws), wsb, _stream(stream)))
+    return y
+
+
+def make_call(op, A, in0=None, in1=None, out0=None, out1=None, B=None, alpha=0.0, beta=0.0,
+              ws=None, stream=None, flush_buf=None) -> MepCall:
+    """A mep_call_t over torch tensors (kept alive by the caller)."""
+    m, n = A.shape
+    ws, wsb = _ws(op, A, ws)
+    c = MepCall()
+    c.op, c.dtype, c.m, c.n = op, dtype_code(A.dtype), m, n
+    c.A, c.B = _ptr(A), _ptr(B)
+    c.in0, c.in1, c.out0, c.out1 = _ptr(in0), _ptr(in1), _ptr(out0), _ptr(out1)
+    c.alpha, c.beta = float(alpha), float(beta)
+    c.ws, c.ws_bytes = _ptr(ws), wsb
+    c.stream = _stream(stream)
+    if flush_buf is not None:
+        c.flush_buf = _ptr(flush_buf)
+        c.flush_bytes = flush_buf.numel() * flush_buf.element_size()
+    c._keep = ws  # the workspace must outlive the call
+    return c
+
+
+def mep_run(call: MepCall) -> None:
+    _check(lib().mep_run(ctypes.byref(call)))
+
+
+def mep_time_trimmed(call: MepCall, warmup: int = 3, R: int = 30, k: int = 3, inner: int = 1,
+                     flush: bool = False):
+    """Eq. 3 timing: returns (trimmed mean ms, list of R sample ms)."""
+    mean = ctypes.c_double()
+    samples = (ctypes.c_double * max(R, 1))()
+    _check(lib().mep_time_trimmed(ctypes.byref(call), warmup, R, k, inner, int(bool(flush)),
+                                  ctypes.byref(mean), samples))
+    return mean.value, list(samples[:R])
+
+
+def mep_trimmed_mean(samples, k: int) -> float:
+    arr = (ctypes.c_double * max(len(samples), 1))(*[float(v) for v in samples])
+    return float(lib().mep_trimmed_mean(arr, len(samples), k))
+
+
+def mep_check_fe(out, ref, tol: float, dtype: Optional[int] = None):
+    """Eq. 4 check of a host output against a host fp64 reference.
+
+    ``out`` is a numpy array (float32/float64) or a torch tensor (copied to
+    the host); returns (error, passed)."""
+    import numpy as np
+
+    if hasattr(out, "detach"):
+        out = out.detach().cpu().numpy()
+    out = np.ascontiguousarray(out)
+    if dtype is None:
+        dtype = MEP_F32 if out.dtype == np.float32 else MEP_F64
+    ref = np.ascontiguousarray(ref, dtype=np.float64)
+    if out.size != ref.size:
+        raise ValueError("out and ref differ in length")
+    err = ctypes.c_double()
+    ok = ctypes.c_int()
+    _check(lib().mep_check_fe(dtype, out.ctypes.data if out.size else None,
+                              ref.ctypes.data_as(ctypes.POINTER(ctypes.c_double)) if ref.size else None,
+                              out.size, float(tol), ctypes.byref(err), ctypes.byref(ok)))
+    return err.value, bool(ok.value)
+
+
+def mep_variant_count(op: int, dtype: int, m: int, n: int) -> int:
+    return int(lib().mep_variant_count(op, dtype, m, n))
+
+
+def mep_set_variant(op: int, variant: int) -> None:
+    _check(lib().mep_set_variant(op, variant))
+
+
+def mep_profile_begin(capacity: int) -> None:
+    _check(lib().mep_profile_begin(capacity))
+
+
+def mep_profile_end():
+    """Returns (summed streaming-kernel ms, number of launches)."""
+    tot = ctypes.c_double()
+    cnt = ctypes.c_int()
+    _check(lib().mep_profile_end(ctypes.byref(tot), ctypes.byref(cnt)))
+    return tot.value, cnt.value
+
+
+def mep_stream_copy(src, dst, stream=None) -> None:
+    nbytes = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() < nbytes:
+        raise ValueError("dst smaller than src")
+    _check(lib().mep_stream_copy(_ptr(src), _ptr(dst), nbytes, _stream(stream)))

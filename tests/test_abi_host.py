@@ -1,0 +1,156 @@
+"""The C-ABI library on the host: symbols, argument checks, host logic.
+
+No kernel runs here: every call below either is host-only (Eq. 3, the FE
+metric, workspace sizing) or fails its argument checks before anything is
+launched.
+"""
+import ctypes
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2512_22147_amd import mep
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mep.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(mep_\w+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    return mep.lib()
+
+
+def test_library_exports_every_declared_function(L):
+    names = declared_functions()
+    assert len(names) == 16
+    for name in names:
+        assert hasattr(L, name), f"{name} not exported"
+    assert sorted(mep.EXPORTS) == names
+
+
+def test_version(L):
+    assert "gfx950" in mep.mep_version()
+
+
+def test_trimmed_mean_matches_eq3():
+    rng = np.random.default_rng(5)
+    for R, k in [(30, 3), (7, 0), (5, 2), (31, 15)]:
+        s = list(rng.exponential(1.0, R))
+        assert mep.mep_trimmed_mean(s, k) == oracle.trimmed_mean(s, k)
+    assert mep.mep_trimmed_mean(list(range(1, 31)), 3) == 15.5
+    assert math.isnan(mep.mep_trimmed_mean([1.0] * 6, 3))
+    assert math.isnan(mep.mep_trimmed_mean([1.0] * 6, -1))
+
+
+@pytest.mark.parametrize("dt", [np.float32, np.float64])
+def test_check_fe_matches_metric(dt):
+    rng = np.random.default_rng(7)
+    ref = rng.standard_normal(1000)
+    for scale in (0.0, 1e-9, 1e-5, 1e-2):
+        out = (ref + scale * rng.standard_normal(1000)).astype(dt)
+        err, ok = mep.mep_check_fe(out, ref, 1e-4)
+        want = oracle.fe_error(out, ref)
+        assert err == pytest.approx(want, rel=1e-12, abs=0.0)
+        assert ok == (want <= 1e-4)
+    bad = ref.astype(dt).copy()
+    bad[17] = np.nan
+    assert mep.mep_check_fe(bad, ref, 1.0) == (math.inf, False)
+    assert mep.mep_check_fe(np.zeros(4, dt), np.zeros(4), 0.0) == (0.0, True)
+    assert mep.mep_check_fe(np.array([0, 1e-30], dt), np.zeros(2), 1.0)[1] is False
+    assert mep.mep_check_fe(np.zeros(0, dt), np.zeros(0), 0.0) == (0.0, True)
+
+
+def test_workspace_sizes():
+    f32, f64 = mep.MEP_F32, mep.MEP_F64
+    ws = mep.mep_workspace_bytes
+    assert ws(mep.MEP_OP_MATVEC, f32, 1000, 1000) == 0           # one panel: no partials
+    assert ws(mep.MEP_OP_ATA_X, f32, 16384, 16384) >= 256 * 16384 * 4
+    assert ws(mep.MEP_OP_ATA_X, f32, 0, 100) == 0
+    assert ws(mep.MEP_OP_ATA_X, f32, 100, 0) == 0
+    assert ws(mep.MEP_OP_MATVEC_T, f64, 1 << 20, 64) > 0
+    assert ws(mep.MEP_OP_ATA_X, f64, 1000, 40000) > 1000 * 8    # two passes keep t
+    assert ws(99, f32, 10, 10) == 0
+    assert ws(mep.MEP_OP_MATVEC, 7, 10, 10) == 0
+    for op in range(5):
+        for dt in (f32, f64):
+            assert mep.mep_variant_count(op, dt, 4096, 4096) >= 1
+    assert mep.mep_variant_count(9, f32, 10, 10) == 0
+
+
+def _rc(fn, *args):
+    rc = fn(*args)
+    return rc, mep.mep_last_error()
+
+
+FAKE = 1 << 20  # an aligned address that is never dereferenced: the checks fail first
+
+
+def test_argument_errors(L):
+    f32 = mep.MEP_F32
+    rc, msg = _rc(L.mep_matvec, 3, 4, 4, FAKE, FAKE, FAKE * 2, None, 0, None)
+    assert rc == mep.MEP_EINVAL and "dtype" in msg
+    rc, msg = _rc(L.mep_matvec, f32, -1, 4, FAKE, FAKE, FAKE * 2, None, 0, None)
+    assert rc == mep.MEP_EINVAL and "negative" in msg
+    rc, msg = _rc(L.mep_matvec, f32, 1 << 31, 4, FAKE, FAKE, FAKE * 2, None, 0, None)
+    assert rc == mep.MEP_EINVAL
+    rc, msg = _rc(L.mep_matvec, f32, 4, 4, None, FAKE, FAKE * 2, None, 0, None)
+    assert rc == mep.MEP_EINVAL and "A" in msg
+    rc, msg = _rc(L.mep_matvec, f32, 4, 4, FAKE + 2, FAKE * 4, FAKE * 2, None, 0, None)
+    assert rc == mep.MEP_EALIGN
+    rc, msg = _rc(L.mep_matvec, mep.MEP_F64, 4, 4, FAKE + 4, FAKE * 4, FAKE * 2, None, 0, None)
+    assert rc == mep.MEP_EALIGN
+    # output overlapping an input
+    rc, msg = _rc(L.mep_matvec, f32, 4, 4, FAKE, FAKE * 4, FAKE + 8, None, 0, None)
+    assert rc == mep.MEP_EINVAL and "overlap" in msg
+    # workspace too small
+    need = mep.mep_workspace_bytes(mep.MEP_OP_ATA_X, f32, 4096, 4096)
+    rc, msg = _rc(L.mep_ata_x, f32, 4096, 4096, FAKE, FAKE * 64, FAKE * 65, None, FAKE * 128,
+                  need - 1, None)
+    assert rc == mep.MEP_EWORKSPACE
+    rc, msg = _rc(L.mep_ata_x, f32, 4096, 4096, FAKE, FAKE * 64, FAKE * 65, None, None, need, None)
+    assert rc == mep.MEP_EWORKSPACE
+    rc, msg = _rc(L.mep_ata_x, f32, 4096, 4096, FAKE, FAKE * 64, FAKE * 65, None, FAKE * 128 + 16,
+                  need, None)
+    assert rc == mep.MEP_EALIGN
+    # BICG needs p and q together
+    rc, msg = _rc(L.mep_matvec_t, f32, 8, 8, FAKE, FAKE * 4, FAKE * 5, FAKE * 6, None, None, 0, None)
+    assert rc == mep.MEP_EINVAL and "p and q" in msg
+    rc, msg = _rc(L.mep_matvec_t, f32, 8, 8, FAKE, FAKE * 4, FAKE * 5, None, FAKE * 6, None, 0, None)
+    assert rc == mep.MEP_EINVAL and "p and q" in msg
+    # two outputs overlapping each other
+    wsb = mep.mep_workspace_bytes(mep.MEP_OP_BICG, f32, 8, 8)
+    rc, msg = _rc(L.mep_matvec_t, f32, 8, 8, FAKE, FAKE * 4, FAKE * 5, FAKE * 6, FAKE * 5 + 16,
+                  FAKE * 128, wsb, None)
+    assert rc == mep.MEP_EINVAL and "overlap" in msg
+    rc, msg = _rc(L.mep_axpby_mv, f32, 8, 8, 1.0, FAKE, 1.0, None, FAKE * 4, FAKE * 5, None, 0, None)
+    assert rc == mep.MEP_EINVAL and "B" in msg
+
+
+def test_harness_errors(L):
+    c = mep.MepCall()
+    c.op, c.dtype, c.m, c.n = mep.MEP_OP_ATA_X, mep.MEP_F32, 8, 8
+    mean = ctypes.c_double()
+    for R, k in [(6, 3), (2, 1), (0, 0)]:
+        assert L.mep_time_trimmed(ctypes.byref(c), 0, R, k, 1, 0, ctypes.byref(mean), None) == mep.MEP_EBUDGET
+    assert L.mep_time_trimmed(ctypes.byref(c), 0, 30, 3, 0, 0, ctypes.byref(mean), None) == mep.MEP_EBUDGET
+    assert L.mep_time_trimmed(None, 0, 30, 3, 1, 0, ctypes.byref(mean), None) == mep.MEP_EINVAL
+    c.op = 42
+    assert L.mep_run(ctypes.byref(c)) == mep.MEP_EINVAL
+    c.op = mep.MEP_OP_BICG
+    assert L.mep_run(ctypes.byref(c)) == mep.MEP_EINVAL
+    assert L.mep_set_variant(17, 0) == mep.MEP_EINVAL
+    assert L.mep_profile_begin(0) == mep.MEP_EINVAL
+    assert L.mep_profile_end(None, None) == mep.MEP_EINVAL
+    assert L.mep_stream_copy(FAKE, FAKE * 2, 24, None) == mep.MEP_EALIGN
+    assert L.mep_stream_copy(FAKE, FAKE + 16, 64, None) == mep.MEP_EINVAL
+    assert L.mep_stream_copy(None, None, 0, None) == mep.MEP_OK

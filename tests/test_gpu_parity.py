@@ -1,0 +1,216 @@
+"""GPU kernels (through the C-ABI) against the CPU oracle.
+
+Bar: normwise relative error <= 1e-4 (fp32) / 1e-12 (fp64) on random inputs;
+bit-exact on integer-valued inputs, where every partial sum is an exact
+integer in either precision; bitwise run-to-run reproducibility.
+"""
+import numpy as np
+import pytest
+
+from tests.gpu_cases import (OPS, assert_parity, gpu_outputs, make_inputs, op_code,
+                             oracle_outputs)
+
+pytestmark = pytest.mark.gpu
+
+DTYPES = [np.float32, np.float64]
+
+
+@pytest.fixture(autouse=True)
+def _gpu():
+    import torch
+
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2512_22147_amd import mep
+
+    for op in range(5):
+        mep.mep_set_variant(op, -1)
+    yield
+    for op in range(5):
+        mep.mep_set_variant(op, -1)
+
+
+# shapes chosen to cover every row-group width, ragged tails of rows and of
+# row vectors, several workgroups and several tiles
+EDGE_SHAPES = [(1, 1), (1, 7), (7, 1), (3, 5), (63, 63), (64, 64), (65, 129), (100, 1000),
+               (257, 4100), (1000, 1024), (37, 16388), (300, 8192), (129, 16384)]
+
+
+@pytest.mark.parametrize("dt", DTYPES, ids=["f32", "f64"])
+@pytest.mark.parametrize("op", OPS)
+@pytest.mark.parametrize("shape", EDGE_SHAPES, ids=lambda s: f"{s[0]}x{s[1]}")
+def test_edge_shapes_every_candidate(op, shape, dt):
+    from paper_2512_22147_amd import mep
+
+    m, n = shape
+    ins = make_inputs(op, m, n, dt, seed=1000 + m + 7 * n)
+    ref = oracle_outputs(op, ins, dt)
+    code = op_code(op)
+    count = mep.mep_variant_count(code, mep.MEP_F32 if dt == np.float32 else mep.MEP_F64, m, n)
+    assert count >= 1
+    for v in range(count):
+        mep.mep_set_variant(code, v)
+        got = gpu_outputs(op, ins, dt)
+        assert_parity(op, got, ref, dt, what=f"{m}x{n} candidate {v}")
+
+
+@pytest.mark.parametrize("dt", DTYPES, ids=["f32", "f64"])
+@pytest.mark.parametrize("op", OPS)
+@pytest.mark.parametrize("shape", [(2048, 4096), (513, 1027), (4000, 64), (3, 40000)],
+                         ids=lambda s: f"{s[0]}x{s[1]}")
+def test_integer_inputs_bit_exact(op, shape, dt):
+    """Entries in {-1, 0, 1}: every partial sum is an integer below 2^24, so
+    any summation order gives the exact result, in fp32 as in fp64."""
+    m, n = shape
+    ins = make_inputs(op, m, n, dt, seed=77 + m, kind="ternary")
+    ref = oracle_outputs(op, ins, dt, alpha=1.5, beta=0.25)
+    got = gpu_outputs(op, ins, dt, alpha=1.5, beta=0.25)
+    for k, r in ref.items():
+        assert np.array_equal(got[k].astype(np.float64), r), f"{op} {k} not exact"
+
+
+@pytest.mark.parametrize("dt", DTYPES, ids=["f32", "f64"])
+@pytest.mark.parametrize("op", OPS)
+def test_long_rows_use_column_panels(op, dt):
+    """Rows longer than one on-chip row group: column panels (and for ATAX
+    the two-pass path)."""
+    n = 40000 if dt == np.float32 else 20000
+    for m in (1, 67):
+        ins = make_inputs(op, m, n, dt, seed=5 + m)
+        assert_parity(op, gpu_outputs(op, ins, dt), oracle_outputs(op, ins, dt), dt,
+                      what=f"{m}x{n}")
+
+
+@pytest.mark.parametrize("dt", DTYPES, ids=["f32", "f64"])
+@pytest.mark.parametrize("op", OPS)
+def test_misaligned_matrix_takes_elementwise_path(op, dt):
+    import torch
+
+    from paper_2512_22147_amd import mep
+
+    m, n = 70, 516
+    ins = make_inputs(op, m, n, dt, seed=9)
+    ref = oracle_outputs(op, ins, dt)
+    dev = torch.device("cuda:0")
+    # A (and B) start one element past a 16-byte boundary
+    raw = torch.empty(m * n + 1, dtype=torch.float32 if dt == np.float32 else torch.float64,
+                      device=dev)
+    A = raw[1:].view(m, n)
+    A.copy_(torch.from_numpy(ins["A"]))
+    assert A.data_ptr() % 16 != 0
+    x = torch.from_numpy(ins.get("x", np.zeros(n, dt))).to(dev)
+    if op == "matvec":
+        got = {"y": mep.mep_matvec(A, x)}
+    elif op == "matvec_t":
+        got = {"z": mep.mep_matvec_t(A, torch.from_numpy(ins["w"]).to(dev))}
+    elif op == "bicg":
+        z, q = mep.mep_matvec_t(A, torch.from_numpy(ins["w"]).to(dev), p=x)
+        got = {"z": z, "q": q}
+    elif op == "ata_x":
+        t = torch.empty(m, dtype=A.dtype, device=dev)
+        got = {"y": mep.mep_ata_x(A, x, t=t), "t": t}
+    else:
+        rawb = torch.empty_like(raw)
+        Bm = rawb[1:].view(m, n)
+        Bm.copy_(torch.from_numpy(ins["B"]))
+        got = {"y": mep.mep_axpby_mv(1.5, A, 1.2, Bm, x)}
+    torch.cuda.synchronize()
+    assert_parity(op, {k: v.cpu().numpy() for k, v in got.items()}, ref, dt)
+
+
+@pytest.mark.parametrize("dt", DTYPES, ids=["f32", "f64"])
+def test_empty_sizes(dt):
+    """An empty sum is zero; zero-length outputs are left alone."""
+    import torch
+
+    from paper_2512_22147_amd import mep
+
+    dev = torch.device("cuda:0")
+    tdt = torch.float32 if dt == np.float32 else torch.float64
+    e = lambda *s: torch.empty(*s, dtype=tdt, device=dev)
+    A0n = e(0, 5)
+    Am0 = e(6, 0)
+    assert mep.mep_matvec(Am0, e(0), y=torch.full((6,), 7.0, dtype=tdt, device=dev)).abs().sum() == 0
+    assert mep.mep_matvec(A0n, e(5)).numel() == 0
+    assert mep.mep_matvec_t(A0n, e(0), z=torch.full((5,), 7.0, dtype=tdt, device=dev)).abs().sum() == 0
+    z, q = mep.mep_matvec_t(Am0, e(6), p=e(0), q=torch.full((6,), 7.0, dtype=tdt, device=dev))
+    assert z.numel() == 0 and q.abs().sum() == 0
+    assert mep.mep_ata_x(A0n, e(5), y=torch.full((5,), 7.0, dtype=tdt, device=dev)).abs().sum() == 0
+    t = torch.full((6,), 7.0, dtype=tdt, device=dev)
+    mep.mep_ata_x(Am0, e(0), t=t)
+    assert t.abs().sum() == 0
+    assert mep.mep_axpby_mv(1.0, Am0, 1.0, e(6, 0), e(0),
+                            y=torch.full((6,), 7.0, dtype=tdt, device=dev)).abs().sum() == 0
+    torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("op", OPS)
+def test_guards_and_reproducibility(op):
+    """Nothing is written past the outputs or the workspace, and two runs give
+    bitwise-identical results (fixed-order reductions, no atomics)."""
+    import torch
+
+    from paper_2512_22147_amd import mep
+
+    dt = np.float32
+    m, n = 3000, 4100
+    ins = make_inputs(op, m, n, dt, seed=31)
+    dev = torch.device("cuda:0")
+    T = {k: torch.from_numpy(v).to(dev) for k, v in ins.items()}
+    code = op_code(op)
+    need = mep.mep_workspace_bytes(code, mep.MEP_F32, m, n)
+    G = 4096
+    guard = 0x5A
+    ws_all = torch.full((need + G,), guard, dtype=torch.uint8, device=dev)
+    ws = ws_all[:need] if need else None
+    out_len = {"matvec": m, "matvec_t": n, "bicg": n, "ata_x": n, "axpby_mv": m}[op]
+    sentinel = 12345.0
+    runs = []
+    for _ in range(2):
+        o = torch.full((out_len + G,), sentinel, dtype=torch.float32, device=dev)
+        q = torch.full((m + G,), sentinel, dtype=torch.float32, device=dev)
+        y = o[:out_len]
+        if op == "matvec":
+            mep.mep_matvec(T["A"], T["x"], y=y, ws=ws)
+        elif op == "matvec_t":
+            mep.mep_matvec_t(T["A"], T["w"], z=y, ws=ws)
+        elif op == "bicg":
+            mep.mep_matvec_t(T["A"], T["w"], z=y, p=T["x"], q=q[:m], ws=ws)
+        elif op == "ata_x":
+            mep.mep_ata_x(T["A"], T["x"], y=y, t=q[:m], ws=ws)
+        else:
+            mep.mep_axpby_mv(1.5, T["A"], 1.2, T["B"], T["x"], y=y, ws=ws)
+        torch.cuda.synchronize()
+        assert bool((o[out_len:] == sentinel).all()), "write past the output"
+        assert bool((q[m:] == sentinel).all()), "write past the second output"
+        assert bool((ws_all[need:] == guard).all()), "write past the workspace"
+        runs.append(torch.cat([y, q[:m]]).cpu().numpy())
+    assert np.array_equal(runs[0].view(np.uint32), runs[1].view(np.uint32))
+
+
+def test_harness_on_gpu():
+    """mep_time_trimmed (Eq. 3), profiling events and the copy probe."""
+    import torch
+
+    from paper_2512_22147_amd import mep
+
+    dev = torch.device("cuda:0")
+    m, n = 2048, 2048
+    A = torch.randn(m, n, device=dev)
+    x = torch.randn(n, device=dev)
+    y = torch.empty(n, device=dev)
+    flush = torch.empty(64 << 20, dtype=torch.uint8, device=dev)
+    call = mep.make_call(mep.MEP_OP_ATA_X, A, in0=x, out0=y, flush_buf=flush)
+    mean, samples = mep.mep_time_trimmed(call, warmup=2, R=9, k=2, inner=3, flush=True)
+    assert len(samples) == 9 and all(s > 0 for s in samples)
+    assert mean == pytest.approx(mep.mep_trimmed_mean(samples, 2), rel=1e-12)
+    mep.mep_profile_begin(8)
+    for _ in range(5):
+        mep.mep_run(call)
+    tot, cnt = mep.mep_profile_end()
+    assert cnt == 5 and tot > 0
+    src = torch.arange(1 << 20, dtype=torch.int32, device=dev)
+    dst = torch.zeros_like(src)
+    mep.mep_stream_copy(src, dst)
+    torch.cuda.synchronize()
+    assert torch.equal(src, dst)
