@@ -32,29 +32,28 @@ if ROOT not in sys.path:
 METRIC = "achieved HBM GB/s (and % of MI355X peak) for y=Aᵀ(Ax), fp32 16384²"
 PEAK_GBS = 8000.0
 WORKLOAD = "ata_x_16384"
-KERNEL_SOURCES = ["paper_2512_22147_amd/csrc/mep_kernels.hpp",
-                  "paper_2512_22147_amd/csrc/mep_launch.inc",
-                  "paper_2512_22147_amd/csrc/mep_internal.hpp"]
+KERNEL_SOURCE = "paper_2512_22147_amd/csrc/mep_kernels.hpp"
 TRAFFIC_FILE = "profiles/ata_x_16384_traffic.md"
 
 
 def kernel_source_hash() -> str:
-    h = hashlib.sha256()
-    for rel in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, rel), "rb") as f:
-            h.update(f.read())
-    return h.hexdigest()[:16]
+    with open(os.path.join(ROOT, KERNEL_SOURCE), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def measured_traffic(dtype: str):
-    """HBM bytes per launch of the streaming kernel from the committed
-    rocprofv3 counter summary, or None when absent or taken on other code."""
+def measured_traffic(dtype: str, config: str):
+    """HBM bytes (fetched + written) per launch of the streaming kernel from
+    the committed rocprofv3 counter summary; None when the summary is absent
+    or was taken on another kernel source or another configuration."""
     path = os.path.join(ROOT, TRAFFIC_FILE)
     if not os.path.exists(path):
         return None
     text = open(path).read()
     m = re.search(r"kernel_source_sha256_16:\s*([0-9a-f]+)", text)
     if not m or m.group(1) != kernel_source_hash():
+        return None
+    m = re.search(rf"config_{dtype}:\s*(.+)", text)
+    if not m or m.group(1).strip() != config:
         return None
     m = re.search(rf"traffic_bytes_per_launch_{dtype}:\s*([0-9.eE+]+)", text)
     return float(m.group(1)) if m else None
@@ -111,6 +110,8 @@ def run_gpu(dtype: str, steps: int, warmup: int, variant: int):
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     kern_ms, launches = mep.mep_profile_end()
+    config = mep.mep_variant_info(mep.MEP_OP_ATA_X, mep.dtype_code(A.dtype), m, n,
+                                  max(variant, 0))
     mep.mep_set_variant(mep.MEP_OP_ATA_X, -1)
     alg_step = (m * n + n + n) * es          # A, x, y once
     alg_kernel = (m * n + n) * es            # what the streaming kernel must read
@@ -121,7 +122,7 @@ def run_gpu(dtype: str, steps: int, warmup: int, variant: int):
         "value_gbs": alg_step / (ms_step * 1e-3) / 1e9,
         "kernel_ms": kavg_ms, "kernel_launches": launches,
         "kernel_gbs": alg_kernel / (kavg_ms * 1e-3) / 1e9,
-        "alg_bytes_step": alg_step, "alg_bytes_kernel": alg_kernel,
+        "alg_bytes_step": alg_step, "alg_bytes_kernel": alg_kernel, "config": config,
         "y": y.cpu().numpy(), "A_host": ins["A"], "x_host": ins["x"],
     }
     del A, x, y, ws
@@ -206,10 +207,11 @@ def main():
             "ms_per_step": round(sec["ms_per_step"], 4),
             "kernel_gbs": round(sec["kernel_gbs"], 1),
             "frac_of_peak": round(sec["kernel_gbs"] / PEAK_GBS, 4),
-            "traffic": measured_traffic("f64"),
+            "traffic": measured_traffic("f64", sec["config"]),
+            "kernel_config": sec["config"],
         }
     copy = probe_copy() if args.probe_copy else None
-    traffic = measured_traffic(args.dtype)
+    traffic = measured_traffic(args.dtype, prim["config"])
     out = {
         "metric": METRIC,
         "value": round(prim["value_gbs"], 1),
@@ -229,7 +231,8 @@ def main():
         "roofline": {
             "bound": "hbm", "achieved": round(prim["kernel_gbs"], 1), "peak": PEAK_GBS, "unit": "GB/s",
             "frac": round(prim["kernel_gbs"] / PEAK_GBS, 4), "traffic": traffic,
-            "kernel": "k_stream (ATAX mode)", "kernel_ms": round(prim["kernel_ms"], 5),
+            "kernel": "k_stream (ATAX mode)", "kernel_config": prim["config"],
+            "kernel_ms": round(prim["kernel_ms"], 5),
             "alg_bytes_per_launch": prim["alg_bytes_kernel"],
         },
         "cpu_baseline": cpu,

@@ -181,11 +181,18 @@ int mep_check_fe(int dtype, const void* out, const double* ref, int64_t len, dou
  */
 int mep_variant_count(int op, int dtype, int64_t m, int64_t n);
 int mep_set_variant(int op, int variant);
+/* Writes a short description of candidate `variant` for the shape into buf
+ * (at most buf_len bytes, NUL-terminated): lanes per row group, vectors per
+ * lane, rows per batch, waves per SIMD, load policy, grid.  Returns MEP_OK,
+ * or MEP_EINVAL for a bad op, dtype, shape or variant. */
+int mep_variant_info(int op, int dtype, int64_t m, int64_t n, int variant, char* buf, size_t buf_len);
 
 /*
  * Device-time instrumentation of the dominant (matrix-streaming) kernel.
  * mep_profile_begin(cap) arms up to cap records; while armed, every operation
- * records a HIP event pair around its streaming kernel on its own stream.
+ * launches its streaming kernel with a HIP event pair that the launch itself
+ * stamps at the kernel's start and end (hipExtLaunchKernel), on the kernel's
+ * own stream, so the timing adds no work to the stream.
  * mep_profile_end() synchronizes those events, returns the number of
  * recorded launches and their summed duration, and disarms.  Not thread-safe.
  */

@@ -28,7 +28,8 @@ HIP_FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-I", INCLUDE, "-I", CSRC,
 ]
-SOURCES = ["mep_api.hip", "mep_launch_f32.hip", "mep_launch_f64.hip"]
+SOURCES = ["mep_api.hip", "mep_launch_f32.hip", "mep_launch_f64.hip", "mep_launch_f32_wide.hip",
+           "mep_launch_f64_wide.hip"]
 HEADERS = ["mep_kernels.hpp", "mep_internal.hpp", "mep_launch.inc"]
 
 
@@ -44,7 +45,7 @@ def _run(cmd, verbose):
         print(err, file=sys.stderr)
 
 
-def build_mep(verbose: bool = False, jobs: int = 3) -> str:
+def build_mep(verbose: bool = False, jobs: int = 5) -> str:
     """Compile every HIP source for gfx950 and link libmep.so."""
     os.makedirs(BUILD_DIR, exist_ok=True)
     objs = []

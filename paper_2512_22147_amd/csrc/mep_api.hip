@@ -50,7 +50,33 @@ constexpr int64_t kMaxRow = int64_t(65535) * 8192;
 
 static int esize_of(int dtype) { return dtype == MEP_F32 ? 4 : (dtype == MEP_F64 ? 8 : 0); }
 
-int stream_candidates(int esize, bool vec, int mode, int64_t n, int* idx)
+// The default shape for a row of nv vectors, from measurements on MI355X
+// (candidate sweeps over the five benchmark workloads): the narrowest row
+// group for very short rows, 512-lane groups with 8 or 16 vectors per lane
+// otherwise.  Matrices that stay resident in the 256 MB Infinity Cache across
+// calls are read with cached loads; larger ones are streamed non-temporally.
+static Cfg preferred_shape(int mode, int esize, int64_t m, int64_t n, int64_t nv)
+{
+    const int64_t mats = (mode & F_TWO) ? 2 : 1;
+    const bool stream = mats * m * n * esize > (int64_t(128) << 20);
+    const int aux = stream ? 2 : 0;
+    if (nv <= 16)
+        return Cfg{16, 1, 8, 4, aux};
+    if (nv <= 64)
+        return Cfg{64, 1, 8, 4, aux};
+    if (nv <= 256)
+        return Cfg{64, 4, 2, 4, aux};
+    if (nv <= 4096)
+        return Cfg{512, 8, 2, 2, aux};
+    return Cfg{512, 16, 1, 2, aux};
+}
+
+static bool same_cfg(const Cfg& a, const Cfg& b)
+{
+    return a.G == b.G && a.V == b.V && a.B == b.B && a.WPE == b.WPE && a.AUX == b.AUX;
+}
+
+int stream_candidates(int esize, bool vec, int mode, int64_t m, int64_t n, int* idx)
 {
     const int vw = vec ? 16 / esize : 1;
     const int vgpr32 = vec ? 4 : esize / 4;
@@ -82,13 +108,26 @@ int stream_candidates(int esize, bool vec, int mode, int64_t n, int* idx)
                 (int64_t)tab[i].G * tab[i].V == best)
                 idx[cnt++] = i;
     }
+    // the measured default goes first when it is among the candidates
+    if (vec) {
+        const Cfg want = preferred_shape(mode, esize, m, n, nv);
+        for (int k = 1; k < cnt; ++k) {
+            if (same_cfg(tab[idx[k]], want)) {
+                const int keep = idx[k];
+                for (int j = k; j > 0; --j)
+                    idx[j] = idx[j - 1];
+                idx[0] = keep;
+                break;
+            }
+        }
+    }
     return cnt;
 }
 
 Plan plan_stream(int esize, bool vec, int mode, int64_t m, int64_t n, int variant)
 {
     int idx[16];
-    const int cnt = stream_candidates(esize, vec, mode, n, idx);
+    const int cnt = stream_candidates(esize, vec, mode, m, n, idx);
     const int k = (variant >= 0 && variant < cnt) ? variant : 0;
     Plan p;
     p.vec = vec;
@@ -159,7 +198,7 @@ static size_t ws_bytes_mode(int mode, int esize, int64_t m, int64_t n)
         if (vec && !vec_ok_n(esize, n))
             continue;
         int idx[16];
-        const int cnt = stream_candidates(esize, vec, mode, n, idx);
+        const int cnt = stream_candidates(esize, vec, mode, m, n, idx);
         for (int k = 0; k < cnt; ++k) {
             const Plan p = plan_stream(esize, vec, mode, m, n, k);
             if (mode == MODE_ATAX && p.panels > 1) {
@@ -167,8 +206,8 @@ static size_t ws_bytes_mode(int mode, int esize, int64_t m, int64_t n)
                 size_t s = 0;
                 for (int k2 = 0; k2 < 16; ++k2) {
                     int i1[16], i2[16];
-                    const int c1 = stream_candidates(esize, vec, MODE_MV, n, i1);
-                    const int c2 = stream_candidates(esize, vec, MODE_ATW, n, i2);
+                    const int c1 = stream_candidates(esize, vec, MODE_MV, m, n, i1);
+                    const int c2 = stream_candidates(esize, vec, MODE_ATW, m, n, i2);
                     if (k2 >= c1 && k2 >= c2)
                         break;
                     const Plan p1 = plan_stream(esize, vec, MODE_MV, m, n, k2 < c1 ? k2 : 0);
@@ -265,18 +304,15 @@ struct Prof {
 };
 static Prof g_prof;
 
-static void prof_begin_mark(hipStream_t s)
-{
-    if (g_prof.armed && g_prof.used < g_prof.cap)
-        (void)hipEventRecord(g_prof.start[g_prof.used], s);
-}
-
-static void prof_end_mark(hipStream_t s)
+// The event pair for the next streaming launch while profiling is armed.
+static LaunchEvents prof_next()
 {
     if (g_prof.armed && g_prof.used < g_prof.cap) {
-        (void)hipEventRecord(g_prof.stop[g_prof.used], s);
+        const LaunchEvents ev{g_prof.start[g_prof.used], g_prof.stop[g_prof.used]};
         ++g_prof.used;
+        return ev;
     }
+    return LaunchEvents{nullptr, nullptr};
 }
 
 template <typename T>
@@ -284,10 +320,7 @@ static hipError_t stream_launch(const Plan& p, int mode, const StreamArgs<T>& a,
 {
     if (p.panels > 65535 || p.nb > 65535)
         return hipErrorInvalidConfiguration;  // beyond the grid limits; sizes are checked first
-    prof_begin_mark(s);
-    const hipError_t e = launch_stream<T>(p, mode, a, s);
-    prof_end_mark(s);
-    return e;
+    return launch_stream<T>(p, mode, a, s, prof_next());
 }
 
 static int variant_of(int op) { return g_variant[op].load(std::memory_order_relaxed); }
@@ -540,7 +573,26 @@ int mep_variant_count(int op, int dtype, int64_t m, int64_t n)
         return 0;
     int idx[16];
     const bool vec = vec_ok_n(es, n);
-    return std::max(1, stream_candidates(es, vec, mode, std::max<int64_t>(n, 1), idx));
+    return std::max(1, stream_candidates(es, vec, mode, std::max<int64_t>(m, 1), std::max<int64_t>(n, 1), idx));
+}
+
+int mep_variant_info(int op, int dtype, int64_t m, int64_t n, int variant, char* buf, size_t buf_len)
+{
+    const int es = esize_of(dtype);
+    const int mode = op_mode(op);
+    if (es == 0 || mode < 0 || m < 1 || n < 1 || m > kMaxDim || n > kMaxRow || buf == nullptr ||
+        buf_len == 0)
+        return fail(MEP_EINVAL, "bad arguments to mep_variant_info");
+    const bool vec = vec_ok_n(es, n);
+    int idx[16];
+    const int cnt = stream_candidates(es, vec, mode, m, n, idx);
+    if (variant < 0 || variant >= cnt)
+        return fail(MEP_EINVAL, "variant %d outside 0..%d", variant, cnt - 1);
+    const Plan p = plan_stream(es, vec, mode, m, n, variant);
+    snprintf(buf, buf_len, "%s G=%d V=%d B=%d WPE=%d %s threads=%d grid=%lldx%lld",
+             vec ? "vec16" : "elem", p.c.G, p.c.V, batch_of(p.c.B, mode), p.c.WPE,
+             p.c.AUX ? "nt" : "cached", p.threads, (long long)p.nb, (long long)p.panels);
+    return MEP_OK;
 }
 
 int mep_set_variant(int op, int variant)
@@ -787,10 +839,12 @@ int mep_profile_begin(int capacity)
         return fail(MEP_EINVAL, "profiling is already armed");
     g_prof.start.assign((size_t)capacity, nullptr);
     g_prof.stop.assign((size_t)capacity, nullptr);
+    // no system-scope fence when these events complete: they only time
+    // kernels, nothing on the host reads results through them
     for (int i = 0; i < capacity; ++i) {
-        hipError_t e = hipEventCreate(&g_prof.start[i]);
+        hipError_t e = hipEventCreateWithFlags(&g_prof.start[i], hipEventDisableSystemFence);
         if (e == hipSuccess)
-            e = hipEventCreate(&g_prof.stop[i]);
+            e = hipEventCreateWithFlags(&g_prof.stop[i], hipEventDisableSystemFence);
         if (e != hipSuccess) {
             for (hipEvent_t x : g_prof.start)
                 if (x)

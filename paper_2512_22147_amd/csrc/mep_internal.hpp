@@ -11,21 +11,31 @@
 namespace mep {
 
 // Row-group geometry of one streaming-kernel instance: G lanes per row
-// group, V vectors per lane, B rows per batch, WPE waves per SIMD.
+// group, V vectors per lane, B rows per batch, WPE waves per SIMD (the
+// register budget is 512 / WPE per lane), AUX the cache-policy bits of the
+// matrix loads (0 = default, 2 = non-temporal streaming).
 struct Cfg {
-    int G, V, B, WPE;
+    int G, V, B, WPE, AUX;
 };
 
 // Vector path (16-byte loads), ordered by row capacity G * V; among equal
-// capacities the preferred shape comes first.
-constexpr int kNumVecCfg = 12;
+// capacities the preferred shape comes first (measured on MI355X: streaming
+// the matrix with non-temporal loads is faster for every shape).
+constexpr int kNumVecCfg = 28;
 constexpr Cfg kVecCfg[kNumVecCfg] = {
-    {16, 1, 8, 4},   {64, 1, 8, 4},   {64, 2, 4, 4},  {64, 4, 2, 4},
-    {256, 2, 4, 4},  {256, 4, 2, 4},  {1024, 2, 4, 4}, {1024, 4, 2, 4},
-    {512, 8, 1, 2},  {512, 8, 2, 2},  {512, 16, 1, 2}, {1024, 8, 1, 4}};
+    {16, 1, 8, 4, 2},    {16, 1, 8, 4, 0},    {64, 1, 8, 4, 2},    {64, 1, 8, 4, 0},
+    {64, 2, 4, 4, 2},    {64, 2, 4, 4, 0},    {64, 4, 2, 4, 2},    {64, 4, 2, 4, 0},
+    {256, 2, 4, 4, 2},   {256, 2, 4, 4, 0},   {256, 4, 2, 4, 2},   {256, 4, 2, 4, 0},
+    {1024, 2, 4, 4, 2},  {1024, 2, 4, 4, 0},
+    // 4096 vectors: a 16384-element fp32 row
+    {512, 8, 2, 2, 2},   {1024, 4, 2, 4, 2},  {512, 8, 1, 4, 2},   {256, 16, 1, 2, 2},
+    {512, 8, 2, 2, 0},   {1024, 4, 2, 4, 0},  {512, 8, 1, 4, 0},   {256, 16, 1, 2, 0},
+    // 8192 vectors: a 16384-element fp64 row or a 32768-element fp32 row
+    {512, 16, 1, 2, 2},  {1024, 8, 1, 4, 2},  {256, 32, 1, 1, 2},
+    {512, 16, 1, 2, 0},  {1024, 8, 1, 4, 0},  {256, 32, 1, 1, 0}};
 // Element-wise path (rows not 16-byte aligned): one element per load.
 constexpr int kNumScalarCfg = 3;
-constexpr Cfg kScalarCfg[kNumScalarCfg] = {{64, 4, 2, 4}, {256, 4, 2, 4}, {1024, 8, 1, 4}};
+constexpr Cfg kScalarCfg[kNumScalarCfg] = {{64, 4, 2, 4, 2}, {256, 4, 2, 4, 2}, {1024, 8, 1, 4, 2}};
 
 // Rows per batch an instance really uses: two-matrix modes (GESUMMV) hold
 // twice the rows in registers, so they take half the batch.
@@ -58,14 +68,21 @@ struct Plan {
     int64_t nb;       // row workgroups (gridDim.x)
 };
 
-// Candidate configurations for a row of n elements (a pure function of its
-// arguments: no device query).  Returns the count; fills idx[] (capacity 16).
-int stream_candidates(int esize, bool vec, int mode, int64_t n, int* idx);
+// Candidate configurations for an m x n matrix (a pure function of its
+// arguments: no device query), the default first.  Returns the count; fills
+// idx[] (capacity 16).
+int stream_candidates(int esize, bool vec, int mode, int64_t m, int64_t n, int* idx);
 // The plan of candidate `variant` (-1: the default, candidate 0).
 Plan plan_stream(int esize, bool vec, int mode, int64_t m, int64_t n, int variant);
 
+// Optional timing events for one streaming-kernel launch (both null: none).
+struct LaunchEvents {
+    hipEvent_t start, stop;
+};
+
 template <typename T>
-hipError_t launch_stream(const Plan& p, int mode, const StreamArgs<T>& a, hipStream_t s);
+hipError_t launch_stream(const Plan& p, int mode, const StreamArgs<T>& a, hipStream_t s,
+                         const LaunchEvents& ev);
 
 template <typename T>
 hipError_t launch_colreduce(const T* P, const T* Q, int64_t ldp, int64_t nrows, int64_t ncols,
@@ -74,11 +91,11 @@ hipError_t launch_colreduce(const T* P, const T* Q, int64_t ldp, int64_t nrows, 
 template <typename T>
 hipError_t launch_fill_zero(T* p, int64_t count, hipStream_t s);
 
-// The per-dtype launch tables (mep_launch_f32.hip, mep_launch_f64.hip).
+// The per-dtype launch tables (mep_launch_{f32,f64}{,_wide}.hip).
 template <>
-hipError_t launch_stream<float>(const Plan&, int, const StreamArgs<float>&, hipStream_t);
+hipError_t launch_stream<float>(const Plan&, int, const StreamArgs<float>&, hipStream_t, const LaunchEvents&);
 template <>
-hipError_t launch_stream<double>(const Plan&, int, const StreamArgs<double>&, hipStream_t);
+hipError_t launch_stream<double>(const Plan&, int, const StreamArgs<double>&, hipStream_t, const LaunchEvents&);
 template <>
 hipError_t launch_colreduce<float>(const float*, const float*, int64_t, int64_t, int64_t, float, float,
                                    float*, hipStream_t);

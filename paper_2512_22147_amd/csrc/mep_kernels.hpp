@@ -510,7 +510,26 @@ k_colreduce(const T* __restrict__ P, const T* __restrict__ Q, int64_t ldp, int64
     const vec zero = (vec)(T)0;
     vec s = zero, s2 = zero;
     if (ok) {
-        for (int64_t b = sl; b < nrows; b += SL) {
+        // four rows per step with their loads issued together, still added in
+        // ascending row order
+        constexpr int U = 4;
+        int64_t b = sl;
+        for (; b + (U - 1) * SL < nrows; b += U * SL) {
+            vec t[U], t2[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                t[u] = load_vec<T, VW>(P + (b + u * SL) * ldp + col);
+                if constexpr (TWO)
+                    t2[u] = load_vec<T, VW>(Q + (b + u * SL) * ldp + col);
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                s += t[u];
+                if constexpr (TWO)
+                    s2 += t2[u];
+            }
+        }
+        for (; b < nrows; b += SL) {
             s += load_vec<T, VW>(P + b * ldp + col);
             if constexpr (TWO)
                 s2 += load_vec<T, VW>(Q + b * ldp + col);

@@ -1,0 +1,4 @@
+// fp64 instances of the wide streaming-kernel shapes.
+#define MEP_T double
+#define MEP_WIDE_TABLE
+#include "mep_launch.inc"

@@ -27,7 +27,7 @@ ERROR_NAMES = {1: "MEP_EINVAL", 2: "MEP_EALIGN", 3: "MEP_EWORKSPACE", 4: "MEP_EH
 EXPORTS = (
     "mep_workspace_bytes", "mep_matvec", "mep_matvec_t", "mep_ata_x", "mep_axpby_mv",
     "mep_run", "mep_time_trimmed", "mep_trimmed_mean", "mep_check_fe",
-    "mep_variant_count", "mep_set_variant", "mep_profile_begin", "mep_profile_end",
+    "mep_variant_count", "mep_set_variant", "mep_variant_info", "mep_profile_begin", "mep_profile_end",
     "mep_stream_copy", "mep_last_error", "mep_version",
 )
 
@@ -81,6 +81,7 @@ def lib() -> ctypes.CDLL:
                                ctypes.POINTER(ctypes.c_int)]
     L.mep_variant_count.argtypes = [i, i, i64, i64]
     L.mep_set_variant.argtypes = [i, i]
+    L.mep_variant_info.argtypes = [i, i, i64, i64, i, ctypes.c_char_p, sz]
     L.mep_profile_begin.argtypes = [i]
     L.mep_profile_end.argtypes = [ctypes.POINTER(d), ctypes.POINTER(ctypes.c_int)]
     L.mep_stream_copy.argtypes = [vp, vp, sz, vp]
@@ -265,6 +266,12 @@ def mep_check_fe(out, ref, tol: float, dtype: Optional[int] = None):
 
 def mep_variant_count(op: int, dtype: int, m: int, n: int) -> int:
     return int(lib().mep_variant_count(op, dtype, m, n))
+
+
+def mep_variant_info(op: int, dtype: int, m: int, n: int, variant: int) -> str:
+    buf = ctypes.create_string_buffer(256)
+    _check(lib().mep_variant_info(op, dtype, m, n, variant, buf, 256))
+    return buf.value.decode()
 
 
 def mep_set_variant(op: int, variant: int) -> None:

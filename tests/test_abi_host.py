@@ -32,7 +32,7 @@ def L():
 
 def test_library_exports_every_declared_function(L):
     names = declared_functions()
-    assert len(names) == 16
+    assert len(names) == 17
     for name in names:
         assert hasattr(L, name), f"{name} not exported"
     assert sorted(mep.EXPORTS) == names
@@ -85,6 +85,10 @@ def test_workspace_sizes():
         for dt in (f32, f64):
             assert mep.mep_variant_count(op, dt, 4096, 4096) >= 1
     assert mep.mep_variant_count(9, f32, 10, 10) == 0
+    info = mep.mep_variant_info(mep.MEP_OP_ATA_X, f32, 16384, 16384, 0)
+    assert "G=512" in info and "nt" in info
+    with pytest.raises(mep.MepError):
+        mep.mep_variant_info(mep.MEP_OP_ATA_X, f32, 16384, 16384, 99)
 
 
 def _rc(fn, *args):
