@@ -1,19 +1,23 @@
 #!/usr/bin/env python3
-"""Benchmark of the fused y = A^T (A x) on one MI355X (gfx950).
+"""Benchmark of the dense matrix-vector MEPs on one MI355X (gfx950).
 
-A step is one mep_ata_x call over the 16384 x 16384 workload (uniform[-1,1)
-from seed 3): the matrix-streaming kernel (row dot + transposed accumulation
-in one read of A) and the fixed-order column reduction.  Inputs are resident
-in HBM before timing starts.  One JSON line is printed:
+Default workload: the fused y = A^T (A x) over a 16384 x 16384 fp32 matrix
+(uniform[-1,1) from seed 3).  A step is one call of the operation: for ATAX
+the matrix-streaming kernel (row dot and transposed accumulation in one read
+of A) plus the fixed-order column reduction.  Inputs are resident in HBM
+before timing starts; W warm-up steps, then exactly K timed steps between two
+device synchronizations.  One JSON line is printed:
 
-* value     -- whole-job throughput, algorithmic bytes (A + x + y) per second
-* roofline  -- the streaming kernel's algorithmic bytes (A + x) divided by its
-               average duration, from HIP events recorded around every launch
-               of the timed region on the kernel's own stream
+* value        -- whole-step throughput: algorithmic bytes (every input once,
+                  every output once) per second
+* roofline     -- the dominant kernel's algorithmic bytes per launch divided by
+                  its average duration, from event pairs stamped by each launch
+                  of the timed region on the kernel's own stream; traffic is
+                  the calibrated rocprofv3 HBM byte count per launch
 * cpu_baseline -- the CPU oracle, as it stands, on the host cores
 
-Usage: python bench.py [--steps K] [--warmup W] [--dtype f32|f64]
-                       [--no-cpu-baseline] [--no-f64] [--probe-copy]
+Other workloads (--workload): ata_x_1024, bicg_4096, axpby_mv_8192,
+matvec_t_1m_x_64, reduce_sum_256m, vector_add_256m.
 """
 from __future__ import annotations
 
@@ -29,11 +33,10 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
-METRIC = "achieved HBM GB/s (and % of MI355X peak) for y=Aᵀ(Ax), fp32 16384²"
+HEADLINE = "ata_x_16384"
+HEADLINE_METRIC = "achieved HBM GB/s (and % of MI355X peak) for y=Aᵀ(Ax), fp32 16384²"
 PEAK_GBS = 8000.0
-WORKLOAD = "ata_x_16384"
 KERNEL_SOURCE = "paper_2512_22147_amd/csrc/mep_kernels.hpp"
-TRAFFIC_FILE = "profiles/ata_x_16384_traffic.md"
 
 
 def kernel_source_hash() -> str:
@@ -41,11 +44,11 @@ def kernel_source_hash() -> str:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def measured_traffic(dtype: str, config: str):
-    """HBM bytes (fetched + written) per launch of the streaming kernel from
-    the committed rocprofv3 counter summary; None when the summary is absent
-    or was taken on another kernel source or another configuration."""
-    path = os.path.join(ROOT, TRAFFIC_FILE)
+def measured_traffic(workload: str, dtype: str, config: str):
+    """HBM bytes (fetched + written) per launch of the dominant kernel from the
+    committed rocprofv3 counter summary; None when the summary is absent or was
+    taken on another kernel source or another configuration."""
+    path = os.path.join(ROOT, "profiles", f"{workload}_traffic.md")
     if not os.path.exists(path):
         return None
     text = open(path).read()
@@ -64,6 +67,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default=HEADLINE)
     ap.add_argument("--dtype", choices=["f32", "f64"], default="f32")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-f64", action="store_true", help="skip the fp64 secondary measurement")
@@ -77,55 +81,128 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def run_gpu(dtype: str, steps: int, warmup: int, variant: int):
+OPS = {
+    # workload op -> (mep op code attribute, dominant kernel, description)
+    "ata_x": ("MEP_OP_ATA_X", "k_stream (ATAX mode)", "y = A^T (A x)"),
+    "bicg": ("MEP_OP_BICG", "k_stream (BICG mode)", "q = A p and s = A^T r"),
+    "axpby_mv": ("MEP_OP_AXPBY_MV", "k_stream (AXPBY mode)", "y = alpha A x + beta B x"),
+    "matvec_t": ("MEP_OP_MATVEC_T", "k_stream (A^T w mode)", "z = A^T w"),
+    "reduce_sum": ("MEP_OP_REDUCE_SUM", "k_reduce_sum", "s = sum x"),
+    "vector_add": ("MEP_OP_VECTOR_ADD", "k_vector_add", "c = a + b"),
+}
+
+
+def setup(workload: str, dtype: str):
+    """Device inputs, one step as a closure, and the byte counts."""
     import numpy as np
     import torch
 
     from paper_2512_22147_amd import datagen, mep
 
+    w = datagen.WORKLOADS[workload]
     npdt = np.float32 if dtype == "f32" else np.float64
-    w = datagen.WORKLOADS[WORKLOAD]
-    m, n = w.m, w.n
     es = np.dtype(npdt).itemsize
-    log(f"[bench] generating {WORKLOAD} {dtype} ({m}x{n}, seed {w.seed})")
-    ins = datagen.make_inputs(w, npdt)
+    log(f"[bench] generating {workload} {dtype}")
+    host = datagen.make_inputs(w, npdt)
     dev = torch.device("cuda:0")
-    A = torch.from_numpy(ins["A"]).to(dev)
-    x = torch.from_numpy(ins["x"]).to(dev)
-    y = torch.empty(n, dtype=A.dtype, device=dev)
-    need = mep.mep_workspace_bytes(mep.MEP_OP_ATA_X, mep.dtype_code(A.dtype), m, n)
+    d = {k: torch.from_numpy(v).to(dev) for k, v in host.items()}
+    m, n = w.m, w.n
+    code = getattr(mep, OPS[w.op][0])
+    tdt = d[next(iter(d))].dtype
+    need = mep.mep_workspace_bytes(code, mep.dtype_code(tdt), m, n)
     ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
-    mep.mep_set_variant(mep.MEP_OP_ATA_X, variant)
+    if w.op == "ata_x":
+        y = torch.empty(n, dtype=tdt, device=dev)
+        step = lambda s: mep.mep_ata_x(d["A"], d["x"], y=y, ws=ws, stream=s)
+        outs = lambda: {"y": y}
+        alg_step, alg_kernel = (m * n + 2 * n) * es, (m * n + n) * es
+    elif w.op == "bicg":
+        z = torch.empty(n, dtype=tdt, device=dev)
+        q = torch.empty(m, dtype=tdt, device=dev)
+        step = lambda s: mep.mep_matvec_t(d["A"], d["r"], z=z, p=d["p"], q=q, ws=ws, stream=s)
+        outs = lambda: {"q": q, "s": z}
+        alg_step, alg_kernel = (m * n + 2 * n + 2 * m) * es, (m * n + n + 2 * m) * es
+    elif w.op == "axpby_mv":
+        y = torch.empty(m, dtype=tdt, device=dev)
+        step = lambda s: mep.mep_axpby_mv(w.alpha, d["A"], w.beta, d["B"], d["x"], y=y, ws=ws, stream=s)
+        outs = lambda: {"y": y}
+        alg_step = alg_kernel = (2 * m * n + n + m) * es
+    elif w.op == "matvec_t":
+        z = torch.empty(n, dtype=tdt, device=dev)
+        step = lambda s: mep.mep_matvec_t(d["A"], d["w"], z=z, ws=ws, stream=s)
+        outs = lambda: {"z": z}
+        alg_step, alg_kernel = (m * n + m + n) * es, (m * n + m) * es
+    elif w.op == "reduce_sum":
+        sv = torch.empty(1, dtype=tdt, device=dev)
+        step = lambda s: mep.mep_reduce_sum(d["x"], s=sv, ws=ws, stream=s)
+        outs = lambda: {"s": sv}
+        alg_step, alg_kernel = (n + 1) * es, n * es
+    else:
+        c = torch.empty(n, dtype=tdt, device=dev)
+        step = lambda s: mep.mep_vector_add(d["a"], d["b"], c=c, stream=s)
+        outs = lambda: {"c": c}
+        alg_step = alg_kernel = 3 * n * es
+    return dict(w=w, code=code, step=step, outs=outs, alg_step=alg_step, alg_kernel=alg_kernel,
+                host=host, dev=d, ws=ws, m=m, n=n, tdt=tdt)
+
+
+def oracle_outputs(w, host, dtype):
+    import numpy as np
+
+    import oracle
+
+    if w.op == "ata_x":
+        return {"y": oracle.ata_x(host["A"], host["x"])[0]}
+    if w.op == "bicg":
+        q, s = oracle.bicg(host["A"], host["p"], host["r"])
+        return {"q": q, "s": s}
+    if w.op == "axpby_mv":
+        npdt = np.float32 if dtype == "f32" else np.float64
+        return {"y": oracle.axpby_mv(oracle.elem_scalar(w.alpha, npdt), host["A"],
+                                     oracle.elem_scalar(w.beta, npdt), host["B"], host["x"])}
+    if w.op == "matvec_t":
+        return {"z": oracle.matvec_t(host["A"], host["w"])}
+    if w.op == "reduce_sum":
+        return {"s": np.array([oracle.reduce_sum(host["x"])])}
+    return {"c": oracle.vector_add(host["a"], host["b"])}
+
+
+def run_gpu(workload: str, dtype: str, steps: int, warmup: int, variant: int):
+    import torch
+
+    from paper_2512_22147_amd import mep
+
+    S = setup(workload, dtype)
+    code = S["code"]
+    mep.mep_set_variant(code, variant)
     stream = torch.cuda.current_stream()
     log(f"[bench] warmup {warmup} steps")
     for _ in range(warmup):
-        mep.mep_ata_x(A, x, y=y, ws=ws, stream=stream)
+        S["step"](stream)
     torch.cuda.synchronize()
     mep.mep_profile_begin(steps)
     log(f"[bench] timing {steps} steps")
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(steps):
-        mep.mep_ata_x(A, x, y=y, ws=ws, stream=stream)
+        S["step"](stream)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     kern_ms, launches = mep.mep_profile_end()
-    config = mep.mep_variant_info(mep.MEP_OP_ATA_X, mep.dtype_code(A.dtype), m, n,
-                                  max(variant, 0))
-    mep.mep_set_variant(mep.MEP_OP_ATA_X, -1)
-    alg_step = (m * n + n + n) * es          # A, x, y once
-    alg_kernel = (m * n + n) * es            # what the streaming kernel must read
+    config = mep.mep_variant_info(code, mep.dtype_code(S["tdt"]), S["m"], S["n"], max(variant, 0))
+    mep.mep_set_variant(code, -1)
     ms_step = elapsed * 1e3 / steps
     kavg_ms = kern_ms / max(launches, 1)
     res = {
-        "dtype": dtype, "m": m, "n": n, "ms_per_step": ms_step,
-        "value_gbs": alg_step / (ms_step * 1e-3) / 1e9,
+        "dtype": dtype, "m": S["m"], "n": S["n"], "ms_per_step": ms_step,
+        "value_gbs": S["alg_step"] / (ms_step * 1e-3) / 1e9,
         "kernel_ms": kavg_ms, "kernel_launches": launches,
-        "kernel_gbs": alg_kernel / (kavg_ms * 1e-3) / 1e9,
-        "alg_bytes_step": alg_step, "alg_bytes_kernel": alg_kernel, "config": config,
-        "y": y.cpu().numpy(), "A_host": ins["A"], "x_host": ins["x"],
+        "kernel_gbs": S["alg_kernel"] / (kavg_ms * 1e-3) / 1e9,
+        "alg_bytes_step": S["alg_step"], "alg_bytes_kernel": S["alg_kernel"], "config": config,
+        "outs": {k: v.cpu().numpy() for k, v in S["outs"]().items()},
+        "host": S["host"], "w": S["w"],
     }
-    del A, x, y, ws
+    del S
     torch.cuda.empty_cache()
     return res
 
@@ -153,28 +230,47 @@ def probe_copy():
     return {"bytes_read": nbytes, "bytes_written": nbytes, "gbs": 2 * nbytes / dt / 1e9}
 
 
-def cpu_baseline(A_host, x_host, alg_bytes):
+def cpu_baseline(res):
     import numpy as np
 
     import oracle
 
-    A64 = np.ascontiguousarray(A_host, dtype=np.float64)
-    x64 = np.ascontiguousarray(x_host, dtype=np.float64)
+    w, host = res["w"], res["host"]
+    host64 = {k: np.ascontiguousarray(v, dtype=np.float64) for k, v in host.items()}
     R, k = 3, 1
     times = []
-    y = None
+    ref = None
     log(f"[bench] CPU oracle: {R} calls on {oracle.default().num_threads()} threads")
     for _ in range(R):
         t0 = time.perf_counter()
-        y, _ = oracle.ata_x(A64, x64)
+        ref = oracle_outputs(w, host64, res["dtype"])
         times.append(time.perf_counter() - t0)
     t = oracle.trimmed_mean(times, k)
+    shape = "x".join(str(s) for s in next(iter(host.values())).shape)
     return {
-        "value": alg_bytes / t / 1e9, "unit": "GB/s", "cores": oracle.default().num_threads(),
+        "value": res["alg_bytes_step"] / t / 1e9, "unit": "GB/s", "cores": oracle.default().num_threads(),
         "kind": "oracle", "seconds_per_call": t,
-        "sample": f"the full {A_host.shape[0]}x{A_host.shape[1]} {A_host.dtype} workload (inputs promoted "
-                  f"to fp64 before timing), {R} calls, Eq. 3 trimmed mean with k={k}",
-    }, y
+        "sample": f"the full {w.name} workload ({shape} {res['dtype']}; inputs promoted to fp64 "
+                  f"before timing), {R} calls, Eq. 3 trimmed mean with k={k}",
+    }, ref
+
+
+def fe_vs_oracle(res, ref):
+    import numpy as np
+
+    from paper_2512_22147_amd import mep
+
+    tol = 1e-4 if res["dtype"] == "f32" else 1e-12
+    worst = 0.0
+    for k, r in ref.items():
+        out = res["outs"][k]
+        if res["w"].op == "reduce_sum":
+            # a sum is judged against the size of its terms (it may cancel)
+            scale = float(np.abs(res["host"]["x"].astype(np.float64)).sum())
+            worst = max(worst, abs(float(out[0]) - float(r[0])) / scale)
+        else:
+            worst = max(worst, mep.mep_check_fe(out, r, tol)[0])
+    return worst
 
 
 def main():
@@ -183,37 +279,42 @@ def main():
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the row-sharded "
               "multi-GPU layout is a design, not a measured configuration", file=sys.stderr)
         sys.exit(2)
-    import numpy as np
     import torch
 
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
-    from paper_2512_22147_amd import mep
+    from paper_2512_22147_amd import datagen, mep
 
     mep.lib()
-    prim = run_gpu(args.dtype, args.steps, args.warmup, args.variant)
+    if args.workload not in datagen.WORKLOADS:
+        print(f"unknown workload {args.workload}; known: {sorted(datagen.WORKLOADS)}", file=sys.stderr)
+        sys.exit(2)
+    prim = run_gpu(args.workload, args.dtype, args.steps, args.warmup, args.variant)
     fe = None
     cpu = None
     if not args.no_cpu_baseline:
-        cpu, yref = cpu_baseline(prim["A_host"], prim["x_host"], prim["alg_bytes_step"])
-        fe = mep.mep_check_fe(prim["y"], yref, 1e-4 if args.dtype == "f32" else 1e-12)[0]
+        cpu, ref = cpu_baseline(prim)
+        fe = fe_vs_oracle(prim, ref)
+    prim.pop("host")
     secondary = None
-    if not args.no_f64 and args.dtype == "f32":
-        del prim["A_host"]
-        sec = run_gpu("f64", args.steps, args.warmup, args.variant)
+    if args.workload == HEADLINE and not args.no_f64 and args.dtype == "f32":
+        sec = run_gpu(args.workload, "f64", args.steps, args.warmup, args.variant)
         secondary = {
             "dtype": "f64", "value": round(sec["value_gbs"], 1), "unit": "GB/s",
             "ms_per_step": round(sec["ms_per_step"], 4),
             "kernel_gbs": round(sec["kernel_gbs"], 1),
             "frac_of_peak": round(sec["kernel_gbs"] / PEAK_GBS, 4),
-            "traffic": measured_traffic("f64", sec["config"]),
+            "traffic": measured_traffic(args.workload, "f64", sec["config"]),
             "kernel_config": sec["config"],
         }
     copy = probe_copy() if args.probe_copy else None
-    traffic = measured_traffic(args.dtype, prim["config"])
+    w = prim["w"]
+    desc = OPS[w.op][2]
+    metric = (HEADLINE_METRIC if args.workload == HEADLINE and args.dtype == "f32"
+              else f"achieved HBM GB/s (and % of MI355X peak) for {desc}, {args.dtype} {w.name}")
     out = {
-        "metric": METRIC,
+        "metric": metric,
         "value": round(prim["value_gbs"], 1),
         "unit": "GB/s",
         "n_gpus": 1,
@@ -225,13 +326,14 @@ def main():
         "vs_baseline": None,
         "dtype": args.dtype,
         "data": "synthetic",
-        "config": {"workload": f"y = A^T (A x), A {prim['m']}x{prim['n']} uniform[-1,1) seed 3",
-                   "m": prim["m"], "n": prim["n"], "seed": 3, "kernel_candidate": args.variant},
+        "config": {"workload": f"{desc}, {w.name}: {w.note}; {w.dist} seed {w.seed}",
+                   "m": prim["m"], "n": prim["n"], "seed": w.seed, "kernel_candidate": args.variant},
         "pct_of_peak": round(100.0 * prim["value_gbs"] / PEAK_GBS, 2),
         "roofline": {
             "bound": "hbm", "achieved": round(prim["kernel_gbs"], 1), "peak": PEAK_GBS, "unit": "GB/s",
-            "frac": round(prim["kernel_gbs"] / PEAK_GBS, 4), "traffic": traffic,
-            "kernel": "k_stream (ATAX mode)", "kernel_config": prim["config"],
+            "frac": round(prim["kernel_gbs"] / PEAK_GBS, 4),
+            "traffic": measured_traffic(args.workload, args.dtype, prim["config"]),
+            "kernel": OPS[w.op][1], "kernel_config": prim["config"],
             "kernel_ms": round(prim["kernel_ms"], 5),
             "alg_bytes_per_launch": prim["alg_bytes_kernel"],
         },

@@ -65,7 +65,9 @@ enum {
     MEP_OP_MATVEC_T = 1, /* z = A^T w                                        */
     MEP_OP_BICG = 2,     /* q = A p and s = A^T r, one read of A (BICG)      */
     MEP_OP_ATA_X = 3,    /* y = A^T (A x) (ATAX)                             */
-    MEP_OP_AXPBY_MV = 4  /* y = alpha A x + beta B x (GESUMMV)               */
+    MEP_OP_AXPBY_MV = 4, /* y = alpha A x + beta B x (GESUMMV)               */
+    MEP_OP_REDUCE_SUM = 5, /* s = sum_i x_i ("reduction", Table 3); m = 1    */
+    MEP_OP_VECTOR_ADD = 6  /* c = a + b ("vectoradd", Table 3); m = 1        */
 };
 
 typedef void* mep_stream_t; /* hipStream_t */
@@ -108,12 +110,32 @@ int mep_axpby_mv(int dtype, int64_t m, int64_t n, double alpha, const void* A, d
                  mep_stream_t stream);
 
 /*
+ * s = sum_{i<n} x_i: the "reduction" sample of the AMD APP SDK table (Table 3,
+ * Sec. 4.3).  x: n elements; s: one element of device memory.  Workgroups add
+ * grid-strided shares into partials in ws (mep_workspace_bytes(
+ * MEP_OP_REDUCE_SUM, dtype, 1, n) bytes), which one more kernel adds in a
+ * fixed order: the result is reproducible and no atomics are used.
+ * n = 0 gives s = 0.
+ */
+int mep_reduce_sum(int dtype, int64_t n, const void* x, void* s, void* ws, size_t ws_bytes,
+                   mep_stream_t stream);
+
+/*
+ * c = a + b elementwise: the "vectoradd" sample of Table 3.  a, b, c: n
+ * elements; c must not overlap a or b.  No workspace.
+ */
+int mep_vector_add(int dtype, int64_t n, const void* a, const void* b, void* c,
+                   mep_stream_t stream);
+
+/*
  * One operation, as the MEP harness runs it.  Field use per op:
  *   MATVEC    in0 = x, out0 = y
  *   MATVEC_T  in0 = w, out0 = z
  *   BICG      in0 = r, out0 = s, in1 = p, out1 = q
  *   ATA_X     in0 = x, out0 = y, out1 = t (nullable)
  *   AXPBY_MV  A, B, in0 = x, out0 = y, alpha, beta
+ *   REDUCE_SUM  in0 = x, out0 = s (m = 1, n = length)
+ *   VECTOR_ADD  in0 = a, in1 = b, out0 = c (m = 1, n = length)
  * flush_buf / flush_bytes: optional device buffer the harness overwrites
  * before every timed sample so that no operand stays in the caches.
  */
@@ -188,7 +210,34 @@ int mep_set_variant(int op, int variant);
 int mep_variant_info(int op, int dtype, int64_t m, int64_t n, int variant, char* buf, size_t buf_len);
 
 /*
- * Device-time instrumentation of the dominant (matrix-streaming) kernel.
+ * One round of the candidate selection of Sec. 3.2 over the library's own
+ * kernels for call->op at call's shape: candidate 0 (the default) is the
+ * baseline K^(d); every candidate n runs once and its outputs are compared
+ * with the baseline's by the FE metric of mep_check_fe (Eq. 4, tolerance
+ * tol); each candidate that passes is timed with mep_time_trimmed(warmup, R,
+ * k, inner, flush) (Eq. 3); *best receives the argmin of the trimmed means
+ * over the passing candidates, the lower index on ties (Eq. 5).  With
+ * apply != 0 the winner becomes the op's variant (mep_set_variant), else the
+ * previous setting is restored.  results (nullable, results_cap entries)
+ * receives, per candidate, the trimmed mean (ms; NaN when not timed), the FE
+ * error against the baseline and the FE verdict.  The candidate set is fixed,
+ * so one round is the whole search (the paper's D rounds regenerate
+ * candidates; here nothing new appears in a later round).  Synchronizes
+ * call->stream; overwrites the call's outputs.
+ */
+typedef struct {
+    double mean_ms;
+    double fe_err;
+    int fe_pass;
+} mep_candidate_result_t;
+
+int mep_select_variant(const mep_call_t* call, int warmup, int R, int k, int inner, int flush,
+                       double tol, int apply, int* best, mep_candidate_result_t* results,
+                       int results_cap);
+
+/*
+ * Device-time instrumentation of each operation's dominant kernel (the
+ * matrix-streaming kernel; the first stage of the sum; the vector add).
  * mep_profile_begin(cap) arms up to cap records; while armed, every operation
  * launches its streaming kernel with a HIP event pair that the launch itself
  * stamps at the kernel's start and end (hipExtLaunchKernel), on the kernel's

@@ -11,6 +11,8 @@ Contents
   element summed by one thread in ascending index order.  The paper names these
   kernels (ATAX, BICG, GESUMMV in Tables 1-2, Sec. 4.2) without defining them;
   the textbook definitions are used.
+* ``reduce_sum``, ``vector_add``: the sum of a vector and the elementwise sum
+  of two vectors (the "reduction" and "vectoradd" samples of Table 3), fp64.
 * ``trimmed_mean``: Eq. 3 of Sec. 3.2 -- sort the R samples ascending, drop the
   k lowest and k highest, average the remaining R - 2k; only defined for
   R > 2k.
@@ -64,6 +66,9 @@ class Oracle:
         lib.oracle_bicg.argtypes = [i64, i64, vp, vp, vp, vp, vp]
         lib.oracle_axpby_mv.argtypes = [i64, i64, d, vp, d, vp, vp, vp]
         lib.oracle_num_threads.restype = ctypes.c_int
+        lib.oracle_reduce_sum.argtypes = [i64, vp]
+        lib.oracle_reduce_sum.restype = d
+        lib.oracle_vector_add.argtypes = [i64, vp, vp, vp]
         self.lib = lib
         self.path = lib_path
 
@@ -125,6 +130,18 @@ class Oracle:
         return y
 
 
+    def reduce_sum(self, x) -> float:
+        x = _f64(x).ravel()
+        return float(self.lib.oracle_reduce_sum(x.size, x.ctypes.data))
+
+    def vector_add(self, a, b) -> np.ndarray:
+        a, b = _f64(a).ravel(), _f64(b).ravel()
+        assert a.shape == b.shape
+        c = np.empty(a.size)
+        self.lib.oracle_vector_add(a.size, a.ctypes.data, b.ctypes.data, c.ctypes.data)
+        return c
+
+
 _default = None
 
 
@@ -153,6 +170,14 @@ def bicg(A, p, r):
 
 def axpby_mv(alpha, A, beta, B, x):
     return default().axpby_mv(alpha, A, beta, B, x)
+
+
+def reduce_sum(x):
+    return default().reduce_sum(x)
+
+
+def vector_add(a, b):
+    return default().vector_add(a, b)
 
 
 def elem_scalar(v: float, dtype) -> float:

@@ -19,6 +19,10 @@
  * the set of output elements between threads, so the result is bit-identical
  * for any thread count.
  *
+ * Two further streaming kernels of the paper's AMD APP SDK table (Table 3,
+ * "reduction" and "vectoradd") are defined here too: the sum of a vector and
+ * the elementwise sum of two vectors.
+ *
  * Layout.  A and B are row-major and contiguous, m rows by n columns:
  * A_ij = A[i*n + j].  x, p have length n; w, r, t, q have length m; z, s and
  * the ATAX output y have length n; the outputs of y = A x and of the scaled
@@ -116,4 +120,21 @@ void oracle_axpby_mv(int64_t m, int64_t n, double alpha, const double* A, double
             db += B[i * n + j] * x[j];
         y[i] = alpha * da + beta * db;
     }
+}
+
+/* s = sum_{i=0}^{n-1} x_i, ascending i, in fp64 (the "reduction" sample). */
+double oracle_reduce_sum(int64_t n, const double* x)
+{
+    double s = 0.0;
+    for (int64_t i = 0; i < n; ++i)
+        s += x[i];
+    return s;
+}
+
+/* c_i = a_i + b_i (the "vectoradd" sample), in fp64. */
+void oracle_vector_add(int64_t n, const double* a, const double* b, double* c)
+{
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; ++i)
+        c[i] = a[i] + b[i];
 }

@@ -145,7 +145,7 @@ Plan plan_stream(int esize, bool vec, int mode, int64_t m, int64_t n, int varian
     return p;
 }
 
-static std::atomic<int> g_variant[5] = {{-1}, {-1}, {-1}, {-1}, {-1}};
+static std::atomic<int> g_variant[7] = {{-1}, {-1}, {-1}, {-1}, {-1}, {-1}, {-1}};
 
 static int op_mode(int op)
 {
@@ -160,6 +160,15 @@ static int op_mode(int op)
 }
 
 static size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
+
+// The two vector samples (sum, elementwise add) have no kernel candidates.
+static bool is_vector_op(int op) { return op == MEP_OP_REDUCE_SUM || op == MEP_OP_VECTOR_ADD; }
+
+int64_t reduce_blocks(int64_t n, int esize)
+{
+    const int64_t nv = n * esize / 16;
+    return std::max<int64_t>(1, std::min<int64_t>((nv + 1023) / 1024, 2048));
+}
 
 // Workspace pieces of one plan: column partials (nb rows of n), partial dots
 // of column panels (panels rows of m, twice for two matrices) and, for the
@@ -559,6 +568,11 @@ const char* mep_version(void) { return "mep 0.1 (gfx950)"; }
 size_t mep_workspace_bytes(int op, int dtype, int64_t m, int64_t n)
 {
     const int es = esize_of(dtype);
+    if (is_vector_op(op)) {
+        if (es == 0 || n < 0 || n > kMaxDim || op == MEP_OP_VECTOR_ADD || n == 0)
+            return 0;
+        return align256((size_t)reduce_blocks(n, es) * es);
+    }
     const int mode = op_mode(op);
     if (es == 0 || mode < 0 || m < 0 || n < 0 || m > kMaxDim || n > kMaxDim)
         return 0;
@@ -568,6 +582,8 @@ size_t mep_workspace_bytes(int op, int dtype, int64_t m, int64_t n)
 int mep_variant_count(int op, int dtype, int64_t m, int64_t n)
 {
     const int es = esize_of(dtype);
+    if (is_vector_op(op))
+        return (es == 0 || n < 0 || n > kMaxDim) ? 0 : 1;
     const int mode = op_mode(op);
     if (es == 0 || mode < 0 || m < 0 || n < 0 || m > kMaxDim || n > kMaxDim)
         return 0;
@@ -579,6 +595,16 @@ int mep_variant_count(int op, int dtype, int64_t m, int64_t n)
 int mep_variant_info(int op, int dtype, int64_t m, int64_t n, int variant, char* buf, size_t buf_len)
 {
     const int es = esize_of(dtype);
+    if (is_vector_op(op)) {
+        if (es == 0 || n < 0 || n > kMaxDim || variant != 0 || buf == nullptr || buf_len == 0)
+            return fail(MEP_EINVAL, "bad arguments to mep_variant_info");
+        if (op == MEP_OP_REDUCE_SUM)
+            snprintf(buf, buf_len, "reduce threads=256 grid=%lld, fixed-order partials",
+                     (long long)reduce_blocks(n, es));
+        else
+            snprintf(buf, buf_len, "vector-add threads=256, 16-byte non-temporal");
+        return MEP_OK;
+    }
     const int mode = op_mode(op);
     if (es == 0 || mode < 0 || m < 1 || n < 1 || m > kMaxDim || n > kMaxRow || buf == nullptr ||
         buf_len == 0)
@@ -597,7 +623,7 @@ int mep_variant_info(int op, int dtype, int64_t m, int64_t n, int variant, char*
 
 int mep_set_variant(int op, int variant)
 {
-    if (op_mode(op) < 0)
+    if (op_mode(op) < 0 && !is_vector_op(op))
         return fail(MEP_EINVAL, "unknown op %d", op);
     g_variant[op].store(variant < 0 ? -1 : variant, std::memory_order_relaxed);
     return MEP_OK;
@@ -713,6 +739,56 @@ int mep_axpby_mv(int dtype, int64_t m, int64_t n, double alpha, const void* A, d
                              (double*)y, (char*)ws, s);
 }
 
+int mep_reduce_sum(int dtype, int64_t n, const void* x, void* out, void* ws, size_t ws_bytes,
+                   mep_stream_t stream)
+{
+    int rc = check_sizes(dtype, 1, n);
+    if (rc)
+        return rc;
+    const int es = esize_of(dtype);
+    if ((rc = check_ptr(x, n, es, "x")) || (rc = check_ptr(out, 1, es, "s")))
+        return rc;
+    const size_t need = mep_workspace_bytes(MEP_OP_REDUCE_SUM, dtype, 1, n);
+    if ((rc = check_ws(ws, ws_bytes, need)))
+        return rc;
+    const Range outs[] = {{out, (size_t)es, "s"}};
+    const Range ins[] = {{x, (size_t)n * es, "x"}, {ws, need, "ws"}};
+    if ((rc = check_overlaps(outs, 1, ins, 2)))
+        return rc;
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e;
+    const int64_t nb = reduce_blocks(n, es);
+    if (n == 0)
+        e = dtype == MEP_F32 ? launch_fill_zero<float>((float*)out, 1, s) : launch_fill_zero<double>((double*)out, 1, s);
+    else if (dtype == MEP_F32)
+        e = launch_reduce_sum<float>((const float*)x, n, (float*)out, (float*)ws, nb, s, prof_next());
+    else
+        e = launch_reduce_sum<double>((const double*)x, n, (double*)out, (double*)ws, nb, s, prof_next());
+    return e == hipSuccess ? MEP_OK : hip_fail(e, "reduce launch");
+}
+
+int mep_vector_add(int dtype, int64_t n, const void* a, const void* b, void* c, mep_stream_t stream)
+{
+    int rc = check_sizes(dtype, 1, n);
+    if (rc)
+        return rc;
+    const int es = esize_of(dtype);
+    if ((rc = check_ptr(a, n, es, "a")) || (rc = check_ptr(b, n, es, "b")) || (rc = check_ptr(c, n, es, "c")))
+        return rc;
+    const Range outs[] = {{c, (size_t)n * es, "c"}};
+    const Range ins[] = {{a, (size_t)n * es, "a"}, {b, (size_t)n * es, "b"}};
+    if ((rc = check_overlaps(outs, 1, ins, 2)))
+        return rc;
+    if (n == 0)
+        return MEP_OK;
+    hipStream_t s = (hipStream_t)stream;
+    const LaunchEvents ev = prof_next();
+    const hipError_t e =
+        dtype == MEP_F32 ? launch_vector_add<float>((const float*)a, (const float*)b, (float*)c, n, s, ev)
+                         : launch_vector_add<double>((const double*)a, (const double*)b, (double*)c, n, s, ev);
+    return e == hipSuccess ? MEP_OK : hip_fail(e, "vector add launch");
+}
+
 int mep_run(const mep_call_t* c)
 {
     if (c == nullptr)
@@ -734,6 +810,10 @@ int mep_run(const mep_call_t* c)
     case MEP_OP_AXPBY_MV:
         return mep_axpby_mv(c->dtype, c->m, c->n, c->alpha, c->A, c->beta, c->B, c->in0, c->out0, c->ws,
                             c->ws_bytes, c->stream);
+    case MEP_OP_REDUCE_SUM:
+        return mep_reduce_sum(c->dtype, c->n, c->in0, c->out0, c->ws, c->ws_bytes, c->stream);
+    case MEP_OP_VECTOR_ADD:
+        return mep_vector_add(c->dtype, c->n, c->in0, c->in1, c->out0, c->stream);
     default:
         return fail(MEP_EINVAL, "unknown op %d", c->op);
     }
@@ -801,6 +881,106 @@ int mep_time_trimmed(const mep_call_t* call, int warmup, int R, int k, int inner
     if (samples_ms != nullptr)
         std::memcpy(samples_ms, samples.data(), sizeof(double) * R);
     *mean_ms = mep_trimmed_mean(samples.data(), R, k);
+    return MEP_OK;
+}
+
+// Lengths of a call's two outputs (out0, out1).
+static void output_lengths(const mep_call_t* c, int64_t* l0, int64_t* l1)
+{
+    *l1 = 0;
+    switch (c->op) {
+    case MEP_OP_MATVEC: *l0 = c->m; break;
+    case MEP_OP_MATVEC_T: *l0 = c->n; break;
+    case MEP_OP_BICG: *l0 = c->n; *l1 = c->out1 ? c->m : 0; break;
+    case MEP_OP_ATA_X: *l0 = c->n; *l1 = c->out1 ? c->m : 0; break;
+    case MEP_OP_AXPBY_MV: *l0 = c->m; break;
+    case MEP_OP_REDUCE_SUM: *l0 = 1; break;
+    case MEP_OP_VECTOR_ADD: *l0 = c->n; break;
+    default: *l0 = 0; break;
+    }
+}
+
+// Runs the call once and returns its outputs on the host, promoted to fp64.
+static int run_and_fetch(const mep_call_t* c, std::vector<double>& out)
+{
+    int rc = mep_run(c);
+    if (rc)
+        return rc;
+    hipError_t e = hipStreamSynchronize((hipStream_t)c->stream);
+    if (e != hipSuccess)
+        return hip_fail(e, "synchronize");
+    int64_t l0, l1;
+    output_lengths(c, &l0, &l1);
+    const int es = esize_of(c->dtype);
+    std::vector<char> raw((size_t)(l0 + l1) * es + 1);
+    if (l0 > 0)
+        e = hipMemcpy(raw.data(), c->out0, (size_t)l0 * es, hipMemcpyDeviceToHost);
+    if (e == hipSuccess && l1 > 0)
+        e = hipMemcpy(raw.data() + (size_t)l0 * es, c->out1, (size_t)l1 * es, hipMemcpyDeviceToHost);
+    if (e != hipSuccess)
+        return hip_fail(e, "copy outputs");
+    out.resize((size_t)(l0 + l1));
+    for (int64_t i = 0; i < l0 + l1; ++i)
+        out[i] = es == 4 ? (double)((const float*)raw.data())[i] : ((const double*)raw.data())[i];
+    return MEP_OK;
+}
+
+// The FE metric of mep_check_fe on two host fp64 vectors.
+static double fe_metric(const std::vector<double>& out, const std::vector<double>& ref)
+{
+    double worst = 0.0, scale = 0.0;
+    for (size_t i = 0; i < out.size(); ++i) {
+        if (!std::isfinite(out[i]))
+            return std::numeric_limits<double>::infinity();
+        scale = std::max(scale, std::fabs(ref[i]));
+        worst = std::max(worst, std::fabs(out[i] - ref[i]));
+    }
+    if (scale == 0.0)
+        return worst == 0.0 ? 0.0 : std::numeric_limits<double>::infinity();
+    return worst / scale;
+}
+
+int mep_select_variant(const mep_call_t* call, int warmup, int R, int k, int inner, int flush, double tol,
+                       int apply, int* best, mep_candidate_result_t* results, int results_cap)
+{
+    if (call == nullptr || best == nullptr || (results == nullptr && results_cap > 0) || results_cap < 0)
+        return fail(MEP_EINVAL, "bad arguments to mep_select_variant");
+    if (op_mode(call->op) < 0 && !is_vector_op(call->op))
+        return fail(MEP_EINVAL, "unknown op %d", call->op);
+    if (k < 0 || R <= 2 * k || inner < 1 || warmup < 0)
+        return fail(MEP_EBUDGET, "Eq. 3 needs R > 2k >= 0, inner >= 1, warmup >= 0");
+    const int count = mep_variant_count(call->op, call->dtype, call->m, call->n);
+    if (count < 1)
+        return fail(MEP_EINVAL, "no candidates for this call");
+    const int saved = variant_of(call->op);
+    std::vector<double> base, out;
+    int rc = MEP_OK;
+    int win = -1;
+    double win_ms = 0.0;
+    for (int v = 0; v < count && rc == MEP_OK; ++v) {
+        g_variant[call->op].store(v, std::memory_order_relaxed);
+        mep_candidate_result_t r{std::numeric_limits<double>::quiet_NaN(), 0.0, 0};
+        rc = run_and_fetch(call, v == 0 ? base : out);
+        if (rc)
+            break;
+        r.fe_err = v == 0 ? 0.0 : fe_metric(out, base);
+        r.fe_pass = r.fe_err <= tol ? 1 : 0;
+        if (r.fe_pass) {
+            rc = mep_time_trimmed(call, warmup, R, k, inner, flush, &r.mean_ms, nullptr);
+            if (rc)
+                break;
+            if (win < 0 || r.mean_ms < win_ms) {
+                win = v;
+                win_ms = r.mean_ms;
+            }
+        }
+        if (v < results_cap)
+            results[v] = r;
+    }
+    g_variant[call->op].store(rc == MEP_OK && apply ? win : saved, std::memory_order_relaxed);
+    if (rc)
+        return rc;
+    *best = win;
     return MEP_OK;
 }
 

@@ -107,6 +107,26 @@ hipError_t launch_fill_zero<float>(float*, int64_t, hipStream_t);
 template <>
 hipError_t launch_fill_zero<double>(double*, int64_t, hipStream_t);
 
+// Two-stage sum of n elements (partials in ws, nb = reduce_blocks(n)).
+int64_t reduce_blocks(int64_t n, int esize);
+template <typename T>
+hipError_t launch_reduce_sum(const T* x, int64_t n, T* out, T* partial, int64_t nb, hipStream_t s,
+                             const LaunchEvents& ev);
+template <typename T>
+hipError_t launch_vector_add(const T* a, const T* b, T* c, int64_t n, hipStream_t s, const LaunchEvents& ev);
+template <>
+hipError_t launch_reduce_sum<float>(const float*, int64_t, float*, float*, int64_t, hipStream_t,
+                                    const LaunchEvents&);
+template <>
+hipError_t launch_reduce_sum<double>(const double*, int64_t, double*, double*, int64_t, hipStream_t,
+                                     const LaunchEvents&);
+template <>
+hipError_t launch_vector_add<float>(const float*, const float*, float*, int64_t, hipStream_t,
+                                    const LaunchEvents&);
+template <>
+hipError_t launch_vector_add<double>(const double*, const double*, double*, int64_t, hipStream_t,
+                                     const LaunchEvents&);
+
 hipError_t launch_copy16(const void* src, void* dst, size_t bytes, hipStream_t s);
 hipError_t launch_flush(void* buf, size_t bytes, uint32_t tag, hipStream_t s);
 

@@ -98,7 +98,7 @@ def ternary(seed: int, array_id: int, shape, dtype=np.float32) -> np.ndarray:
 @dataclass(frozen=True)
 class Workload:
     name: str
-    op: str               # "ata_x" | "bicg" | "axpby_mv" | "matvec" | "matvec_t"
+    op: str               # "ata_x" | "bicg" | "axpby_mv" | "matvec" | "matvec_t" | "reduce_sum" | "vector_add"
     m: int
     n: int
     seed: int
@@ -137,6 +137,14 @@ WORKLOADS = {
         (("A", (16384, 16384)), ("x", (16384,))),
         note="fused y = A^T (A x), fp32 (1 GiB) and fp64 (2 GiB), headline",
         dtypes=("f32", "f64")),
+    "reduce_sum_256m": Workload(
+        "reduce_sum_256m", "reduce_sum", 1, 1 << 28, 5, "uniform",
+        (("x", (1 << 28,)),),
+        note="s = sum of x, fp32 (1 GiB): the 'reduction' sample of Table 3"),
+    "vector_add_256m": Workload(
+        "vector_add_256m", "vector_add", 1, 1 << 28, 6, "uniform",
+        (("a", (1 << 28,)), ("b", (1 << 28,))),
+        note="c = a + b, fp32 (2 x 1 GiB in, 1 GiB out): the 'vectoradd' sample of Table 3"),
     "matvec_t_1m_x_64": Workload(
         "matvec_t_1m_x_64", "matvec_t", 1048576, 64, 4, "uniform",
         (("A", (1048576, 64)), ("w", (1048576,))),

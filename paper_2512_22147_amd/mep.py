@@ -20,7 +20,8 @@ LIB_PATH = os.path.join(_HERE, "libmep.so")
 
 MEP_F32, MEP_F64 = 0, 1
 MEP_OK, MEP_EINVAL, MEP_EALIGN, MEP_EWORKSPACE, MEP_EHIP, MEP_EBUDGET = range(6)
-MEP_OP_MATVEC, MEP_OP_MATVEC_T, MEP_OP_BICG, MEP_OP_ATA_X, MEP_OP_AXPBY_MV = range(5)
+(MEP_OP_MATVEC, MEP_OP_MATVEC_T, MEP_OP_BICG, MEP_OP_ATA_X, MEP_OP_AXPBY_MV, MEP_OP_REDUCE_SUM,
+ MEP_OP_VECTOR_ADD) = range(7)
 ERROR_NAMES = {1: "MEP_EINVAL", 2: "MEP_EALIGN", 3: "MEP_EWORKSPACE", 4: "MEP_EHIP", 5: "MEP_EBUDGET"}
 
 # Names exported by libmep.so, in the order include/mep.h declares them.
@@ -28,7 +29,8 @@ EXPORTS = (
     "mep_workspace_bytes", "mep_matvec", "mep_matvec_t", "mep_ata_x", "mep_axpby_mv",
     "mep_run", "mep_time_trimmed", "mep_trimmed_mean", "mep_check_fe",
     "mep_variant_count", "mep_set_variant", "mep_variant_info", "mep_profile_begin", "mep_profile_end",
-    "mep_stream_copy", "mep_last_error", "mep_version",
+    "mep_stream_copy", "mep_last_error", "mep_version", "mep_select_variant",
+    "mep_reduce_sum", "mep_vector_add",
 )
 
 
@@ -51,6 +53,11 @@ class MepCall(ctypes.Structure):
         ("stream", ctypes.c_void_p),
         ("flush_buf", ctypes.c_void_p), ("flush_bytes", ctypes.c_size_t),
     ]
+
+
+class MepCandidateResult(ctypes.Structure):
+    """mep_candidate_result_t."""
+    _fields_ = [("mean_ms", ctypes.c_double), ("fe_err", ctypes.c_double), ("fe_pass", ctypes.c_int)]
 
 
 _lib = None
@@ -85,6 +92,10 @@ def lib() -> ctypes.CDLL:
     L.mep_profile_begin.argtypes = [i]
     L.mep_profile_end.argtypes = [ctypes.POINTER(d), ctypes.POINTER(ctypes.c_int)]
     L.mep_stream_copy.argtypes = [vp, vp, sz, vp]
+    L.mep_reduce_sum.argtypes = [i, i64, vp, vp, vp, sz, vp]
+    L.mep_vector_add.argtypes = [i, i64, vp, vp, vp, vp]
+    L.mep_select_variant.argtypes = [ctypes.POINTER(MepCall), i, i, i, i, i, d, i,
+                                     ctypes.POINTER(ctypes.c_int), ctypes.POINTER(MepCandidateResult), i]
     L.mep_last_error.restype = ctypes.c_char_p
     L.mep_version.restype = ctypes.c_char_p
     _lib = L
@@ -203,13 +214,51 @@ def mep_axpby_mv(alpha, A, beta, B, x, y=None, ws=None, stream=None):
     return y
 
 
+def mep_reduce_sum(x, s=None, ws=None, stream=None):
+    """s = sum of x (one-element tensor)."""
+    torch = _torch()
+    n = x.numel()
+    if s is None:
+        s = torch.empty(1, dtype=x.dtype, device=x.device)
+    need = mep_workspace_bytes(MEP_OP_REDUCE_SUM, dtype_code(x.dtype), 1, n)
+    if ws is None and need > 0:
+        ws = torch.empty(need, dtype=torch.uint8, device=x.device)
+    wsb = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(lib().mep_reduce_sum(dtype_code(x.dtype), n, _ptr(x), _ptr(s), _ptr(ws), wsb,
+                                _stream(stream)))
+    return s
+
+
+def mep_vector_add(a, b, c=None, stream=None):
+    """c = a + b."""
+    torch = _torch()
+    if c is None:
+        c = torch.empty_like(a)
+    _check(lib().mep_vector_add(dtype_code(a.dtype), a.numel(), _ptr(a), _ptr(b), _ptr(c),
+                                _stream(stream)))
+    return c
+
+
 def make_call(op, A, in0=None, in1=None, out0=None, out1=None, B=None, alpha=0.0, beta=0.0,
               ws=None, stream=None, flush_buf=None) -> MepCall:
     """A mep_call_t over torch tensors (kept alive by the caller)."""
-    m, n = A.shape
-    ws, wsb = _ws(op, A, ws)
+    if op in (MEP_OP_REDUCE_SUM, MEP_OP_VECTOR_ADD):
+        # vector samples: A is the first input vector; m = 1, n = its length
+        torch = _torch()
+        m, n = 1, A.numel()
+        in0 = A if in0 is None else in0
+        A = None
+        need = mep_workspace_bytes(op, dtype_code(in0.dtype), m, n)
+        if ws is None and need > 0:
+            ws = torch.empty(need, dtype=torch.uint8, device=in0.device)
+        wsb = 0 if ws is None else ws.numel() * ws.element_size()
+        dt = dtype_code(in0.dtype)
+    else:
+        m, n = A.shape
+        ws, wsb = _ws(op, A, ws)
+        dt = dtype_code(A.dtype)
     c = MepCall()
-    c.op, c.dtype, c.m, c.n = op, dtype_code(A.dtype), m, n
+    c.op, c.dtype, c.m, c.n = op, dt, m, n
     c.A, c.B = _ptr(A), _ptr(B)
     c.in0, c.in1, c.out0, c.out1 = _ptr(in0), _ptr(in1), _ptr(out0), _ptr(out1)
     c.alpha, c.beta = float(alpha), float(beta)
@@ -262,6 +311,18 @@ def mep_check_fe(out, ref, tol: float, dtype: Optional[int] = None):
                               ref.ctypes.data_as(ctypes.POINTER(ctypes.c_double)) if ref.size else None,
                               out.size, float(tol), ctypes.byref(err), ctypes.byref(ok)))
     return err.value, bool(ok.value)
+
+
+def mep_select_variant(call: MepCall, warmup: int = 3, R: int = 30, k: int = 3, inner: int = 1,
+                       flush: bool = False, tol: float = 1e-4, apply: bool = False):
+    """Eqs. 3-5 over the library's candidate kernels; returns (best, per-candidate
+    list of (trimmed mean ms, FE error, FE passed))."""
+    count = mep_variant_count(call.op, call.dtype, call.m, call.n)
+    res = (MepCandidateResult * max(count, 1))()
+    best = ctypes.c_int(-1)
+    _check(lib().mep_select_variant(ctypes.byref(call), warmup, R, k, inner, int(bool(flush)),
+                                    float(tol), int(bool(apply)), ctypes.byref(best), res, count))
+    return best.value, [(r.mean_ms, r.fe_err, bool(r.fe_pass)) for r in res[:count]]
 
 
 def mep_variant_count(op: int, dtype: int, m: int, n: int) -> int:

@@ -268,6 +268,37 @@ def pin_numpy_crosscheck(orc):
         assert _normwise(orc.axpby_mv(1.5, A, 1.2, B, x), 1.5 * (A @ x) + 1.2 * (B @ x)) <= 1e-13
 
 
+def pin_reduce_sum(orc):
+    """Exact rational sums within the recursive-summation bound
+    gamma_{n-1} sum |x_i|; integer inputs exactly; closed forms."""
+    for n, seed in ((1, 71), (2, 72), (17, 73), (100, 74)):
+        x = datagen.uniform(seed, 0, (n,), np.float64)
+        exact = sum((F(v) for v in x), Fraction(0))
+        bound = gamma(max(n - 1, 1)) * sum((abs(F(v)) for v in x), Fraction(0))
+        assert abs(F(orc.reduce_sum(x)) - exact) <= bound, f"reduce_sum n={n}"
+    t = datagen.ternary(75, 0, (100000,), np.float32)
+    assert orc.reduce_sum(t) == float(t.astype(np.int64).sum()), "integer sum"
+    assert orc.reduce_sum(np.ones(12345)) == 12345.0
+    assert orc.reduce_sum(np.zeros(0)) == 0.0
+    assert orc.reduce_sum(np.array([0.5, 0.25, -0.75])) == 0.0
+
+
+def pin_vector_add(orc):
+    """Each sum is one correctly rounded addition: exact for fp32 inputs in
+    fp64, and equal to the exactly rounded rational sum for fp64 inputs."""
+    a = datagen.uniform(81, 0, (1000,), np.float32)
+    b = datagen.uniform(81, 1, (1000,), np.float32)
+    c = orc.vector_add(a, b)
+    assert all(F(ci) == F(ai) + F(bi) for ai, bi, ci in zip(a, b, c)), "fp32 sums exact in fp64"
+    a = datagen.uniform(82, 0, (200,), np.float64)
+    b = datagen.normal(82, 1, (200,), np.float64)
+    c = orc.vector_add(a, b)
+    for ai, bi, ci in zip(a, b, c):
+        e = F(ai) + F(bi)
+        assert abs(F(ci) - e) <= U64 * abs(e), "fp64 sum correctly rounded"
+    assert np.array_equal(orc.vector_add(np.arange(5.0), -np.arange(5.0)), np.zeros(5))
+
+
 ALL_PINS = [
     pin_bruteforce_matvec,
     pin_bruteforce_matvec_t,
@@ -279,4 +310,6 @@ ALL_PINS = [
     pin_closed_forms,
     pin_integer_exact,
     pin_numpy_crosscheck,
+    pin_reduce_sum,
+    pin_vector_add,
 ]

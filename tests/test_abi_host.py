@@ -32,7 +32,7 @@ def L():
 
 def test_library_exports_every_declared_function(L):
     names = declared_functions()
-    assert len(names) == 17
+    assert len(names) == 20
     for name in names:
         assert hasattr(L, name), f"{name} not exported"
     assert sorted(mep.EXPORTS) == names
@@ -85,6 +85,10 @@ def test_workspace_sizes():
         for dt in (f32, f64):
             assert mep.mep_variant_count(op, dt, 4096, 4096) >= 1
     assert mep.mep_variant_count(9, f32, 10, 10) == 0
+    assert mep.mep_workspace_bytes(mep.MEP_OP_REDUCE_SUM, f32, 1, 1 << 28) >= 2048 * 4
+    assert mep.mep_workspace_bytes(mep.MEP_OP_REDUCE_SUM, f32, 1, 0) == 0
+    assert mep.mep_workspace_bytes(mep.MEP_OP_VECTOR_ADD, f64, 1, 1000) == 0
+    assert mep.mep_variant_count(mep.MEP_OP_REDUCE_SUM, f32, 1, 1000) == 1
     info = mep.mep_variant_info(mep.MEP_OP_ATA_X, f32, 16384, 16384, 0)
     assert "G=512" in info and "nt" in info
     with pytest.raises(mep.MepError):
@@ -138,6 +142,14 @@ def test_argument_errors(L):
     assert rc == mep.MEP_EINVAL and "overlap" in msg
     rc, msg = _rc(L.mep_axpby_mv, f32, 8, 8, 1.0, FAKE, 1.0, None, FAKE * 4, FAKE * 5, None, 0, None)
     assert rc == mep.MEP_EINVAL and "B" in msg
+    rc, msg = _rc(L.mep_reduce_sum, f32, 1000, FAKE, FAKE * 4, None, 0, None)
+    assert rc == mep.MEP_EWORKSPACE
+    rc, msg = _rc(L.mep_reduce_sum, f32, 1000, None, FAKE * 4, FAKE * 8, 1 << 16, None)
+    assert rc == mep.MEP_EINVAL
+    rc, msg = _rc(L.mep_vector_add, f32, 1000, FAKE, FAKE * 2, FAKE + 64, None)
+    assert rc == mep.MEP_EINVAL and "overlap" in msg
+    rc, msg = _rc(L.mep_vector_add, mep.MEP_F64, 10, FAKE, FAKE * 2, FAKE * 3 + 4, None)
+    assert rc == mep.MEP_EALIGN
 
 
 def test_harness_errors(L):
@@ -158,3 +170,9 @@ def test_harness_errors(L):
     assert L.mep_stream_copy(FAKE, FAKE * 2, 24, None) == mep.MEP_EALIGN
     assert L.mep_stream_copy(FAKE, FAKE + 16, 64, None) == mep.MEP_EINVAL
     assert L.mep_stream_copy(None, None, 0, None) == mep.MEP_OK
+    best = ctypes.c_int()
+    c.op = mep.MEP_OP_ATA_X
+    assert L.mep_select_variant(ctypes.byref(c), 0, 4, 2, 1, 0, 1e-4, 0, ctypes.byref(best), None, 0) == mep.MEP_EBUDGET
+    assert L.mep_select_variant(None, 0, 30, 3, 1, 0, 1e-4, 0, ctypes.byref(best), None, 0) == mep.MEP_EINVAL
+    c.op = 77
+    assert L.mep_select_variant(ctypes.byref(c), 0, 30, 3, 1, 0, 1e-4, 0, ctypes.byref(best), None, 0) == mep.MEP_EINVAL

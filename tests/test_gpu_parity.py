@@ -214,3 +214,68 @@ def test_harness_on_gpu():
     mep.mep_stream_copy(src, dst)
     torch.cuda.synchronize()
     assert torch.equal(src, dst)
+
+
+FULL = [("ata_x_1024", "f32"), ("bicg_4096", "f32"), ("axpby_mv_8192", "f32"),
+        ("ata_x_16384", "f32"), ("ata_x_16384", "f64"), ("matvec_t_1m_x_64", "f32")]
+
+
+@pytest.mark.parametrize("name,dts", FULL, ids=[f"{a}-{b}" for a, b in FULL])
+def test_full_size_workloads(name, dts):
+    """The benchmark workloads at full size, default kernel candidate (the
+    launch configuration bench.py times), every output element against the
+    oracle; the headline workload also run twice for bitwise equality."""
+    from paper_2512_22147_amd import datagen
+
+    w = datagen.WORKLOADS[name]
+    dt = np.float32 if dts == "f32" else np.float64
+    raw = datagen.make_inputs(w, dt)
+    op = {"ata_x": "ata_x", "bicg": "bicg", "axpby_mv": "axpby_mv", "matvec_t": "matvec_t"}[w.op]
+    if op == "bicg":
+        ins = {"A": raw["A"], "x": raw["p"], "w": raw["r"]}
+    else:
+        ins = dict(raw)
+    ref = oracle_outputs(op, ins, dt, alpha=w.alpha or 1.5, beta=w.beta or 1.2)
+    got = gpu_outputs(op, ins, dt, alpha=w.alpha or 1.5, beta=w.beta or 1.2)
+    assert_parity(op, got, ref, dt, what=name)
+    if name == "ata_x_16384":
+        again = gpu_outputs(op, ins, dt)
+        for k in got:
+            assert np.array_equal(got[k], again[k]), f"{k} differs between runs"
+
+
+@pytest.mark.parametrize("op,shape", [("ata_x", (3000, 4096)), ("matvec_t", (100000, 64)),
+                                      ("axpby_mv", (2000, 2048)), ("bicg", (1024, 1024))])
+def test_select_variant_eqs_3_to_5(op, shape):
+    """The Sec. 3.2 selection over the candidate kernels: every candidate
+    passes FE against the baseline, the winner is the argmin of the Eq. 3
+    means (as the oracle's selection rule computes it from the same list),
+    and once applied the operation still matches the oracle."""
+    import torch
+
+    import oracle
+    from paper_2512_22147_amd import mep
+
+    m, n = shape
+    dt = np.float32
+    ins = make_inputs(op, m, n, dt, seed=404)
+    dev = torch.device("cuda:0")
+    T = {k: torch.from_numpy(v).to(dev) for k, v in ins.items()}
+    code = op_code(op)
+    out0 = torch.empty(m if op in ("matvec", "axpby_mv") else n, device=dev)
+    out1 = torch.empty(m, device=dev) if op in ("bicg", "ata_x") else None
+    kw = dict(out0=out0, out1=out1)
+    if op == "ata_x":
+        call = mep.make_call(code, T["A"], in0=T["x"], **kw)
+    elif op == "bicg":
+        call = mep.make_call(code, T["A"], in0=T["w"], in1=T["x"], **kw)
+    elif op == "matvec_t":
+        call = mep.make_call(code, T["A"], in0=T["w"], out0=out0)
+    else:
+        call = mep.make_call(code, T["A"], in0=T["x"], B=T["B"], alpha=1.5, beta=1.2, out0=out0)
+    best, res = mep.mep_select_variant(call, warmup=1, R=7, k=2, tol=1e-4, apply=True)
+    assert len(res) == mep.mep_variant_count(code, mep.MEP_F32, m, n)
+    assert all(ok for _, _, ok in res), res
+    assert best == oracle.select_next([(i, t, ok) for i, (t, _, ok) in enumerate(res)])
+    got = gpu_outputs(op, ins, dt)
+    assert_parity(op, got, oracle_outputs(op, ins, dt), dt, what=f"selected candidate {best}")

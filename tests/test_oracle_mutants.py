@@ -35,6 +35,10 @@ MUTANTS = {
     "axpby_same_dot_twice": ("y[i] = alpha * da + beta * db;", "y[i] = alpha * da + beta * da;"),
     "axpby_swapped_scalars": ("y[i] = alpha * da + beta * db;", "y[i] = alpha * db + beta * da;"),
     "axpby_reads_A_for_B": ("db += B[i * n + j] * x[j];", "db += A[i * n + j] * x[j];"),
+    "reduce_skips_first": ("for (int64_t i = 0; i < n; ++i)\n        s += x[i];",
+                           "for (int64_t i = 1; i < n; ++i)\n        s += x[i];"),
+    "reduce_fp32_accumulator": ("double s = 0.0;", "float s = 0.0f;"),
+    "vector_add_subtracts": ("c[i] = a[i] + b[i];", "c[i] = a[i] - b[i];"),
 }
 
 RUNNER = r"""
