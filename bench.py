@@ -106,44 +106,47 @@ def setup(workload: str, dtype: str):
     host = datagen.make_inputs(w, npdt)
     dev = torch.device("cuda:0")
     d = {k: torch.from_numpy(v).to(dev) for k, v in host.items()}
+    torch.cuda.synchronize()
     m, n = w.m, w.n
     code = getattr(mep, OPS[w.op][0])
     tdt = d[next(iter(d))].dtype
     need = mep.mep_workspace_bytes(code, mep.dtype_code(tdt), m, n)
     ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    # one prebuilt mep_call_t per workload: a step is a single mep_run call
     if w.op == "ata_x":
         y = torch.empty(n, dtype=tdt, device=dev)
-        step = lambda s: mep.mep_ata_x(d["A"], d["x"], y=y, ws=ws, stream=s)
+        call = mep.make_call(code, d["A"], in0=d["x"], out0=y, ws=ws)
         outs = lambda: {"y": y}
         alg_step, alg_kernel = (m * n + 2 * n) * es, (m * n + n) * es
     elif w.op == "bicg":
         z = torch.empty(n, dtype=tdt, device=dev)
         q = torch.empty(m, dtype=tdt, device=dev)
-        step = lambda s: mep.mep_matvec_t(d["A"], d["r"], z=z, p=d["p"], q=q, ws=ws, stream=s)
+        call = mep.make_call(code, d["A"], in0=d["r"], in1=d["p"], out0=z, out1=q, ws=ws)
         outs = lambda: {"q": q, "s": z}
         alg_step, alg_kernel = (m * n + 2 * n + 2 * m) * es, (m * n + n + 2 * m) * es
     elif w.op == "axpby_mv":
         y = torch.empty(m, dtype=tdt, device=dev)
-        step = lambda s: mep.mep_axpby_mv(w.alpha, d["A"], w.beta, d["B"], d["x"], y=y, ws=ws, stream=s)
+        call = mep.make_call(code, d["A"], in0=d["x"], B=d["B"], alpha=w.alpha, beta=w.beta, out0=y, ws=ws)
         outs = lambda: {"y": y}
         alg_step = alg_kernel = (2 * m * n + n + m) * es
     elif w.op == "matvec_t":
         z = torch.empty(n, dtype=tdt, device=dev)
-        step = lambda s: mep.mep_matvec_t(d["A"], d["w"], z=z, ws=ws, stream=s)
+        call = mep.make_call(code, d["A"], in0=d["w"], out0=z, ws=ws)
         outs = lambda: {"z": z}
         alg_step, alg_kernel = (m * n + m + n) * es, (m * n + m) * es
     elif w.op == "reduce_sum":
         sv = torch.empty(1, dtype=tdt, device=dev)
-        step = lambda s: mep.mep_reduce_sum(d["x"], s=sv, ws=ws, stream=s)
+        call = mep.make_call(code, d["x"], out0=sv, ws=ws)
         outs = lambda: {"s": sv}
         alg_step, alg_kernel = (n + 1) * es, n * es
     else:
         c = torch.empty(n, dtype=tdt, device=dev)
-        step = lambda s: mep.mep_vector_add(d["a"], d["b"], c=c, stream=s)
+        call = mep.make_call(code, d["a"], in1=d["b"], out0=c)
         outs = lambda: {"c": c}
         alg_step = alg_kernel = 3 * n * es
+    step = lambda: mep.mep_run(call)
     return dict(w=w, code=code, step=step, outs=outs, alg_step=alg_step, alg_kernel=alg_kernel,
-                host=host, dev=d, ws=ws, m=m, n=n, tdt=tdt)
+                host=host, dev=d, ws=ws, m=m, n=n, tdt=tdt, call=call)
 
 
 def oracle_outputs(w, host, dtype):
@@ -175,17 +178,16 @@ def run_gpu(workload: str, dtype: str, steps: int, warmup: int, variant: int):
     S = setup(workload, dtype)
     code = S["code"]
     mep.mep_set_variant(code, variant)
-    stream = torch.cuda.current_stream()
     log(f"[bench] warmup {warmup} steps")
     for _ in range(warmup):
-        S["step"](stream)
+        S["step"]()
     torch.cuda.synchronize()
     mep.mep_profile_begin(steps)
     log(f"[bench] timing {steps} steps")
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(steps):
-        S["step"](stream)
+        S["step"]()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     kern_ms, launches = mep.mep_profile_end()

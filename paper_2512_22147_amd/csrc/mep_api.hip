@@ -73,7 +73,7 @@ static Cfg preferred_shape(int mode, int esize, int64_t m, int64_t n, int64_t nv
 
 static bool same_cfg(const Cfg& a, const Cfg& b)
 {
-    return a.G == b.G && a.V == b.V && a.B == b.B && a.WPE == b.WPE && a.AUX == b.AUX;
+    return a.G == b.G && a.V == b.V && a.B == b.B && a.WPE == b.WPE && a.AUX == b.AUX && a.MAP == b.MAP;
 }
 
 int stream_candidates(int esize, bool vec, int mode, int64_t m, int64_t n, int* idx)
@@ -164,10 +164,12 @@ static size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
 // The two vector samples (sum, elementwise add) have no kernel candidates.
 static bool is_vector_op(int op) { return op == MEP_OP_REDUCE_SUM || op == MEP_OP_VECTOR_ADD; }
 
+// Workgroups of the sum: one contiguous chunk of >= 8192 vectors each, at
+// most 512 (two per compute unit: measured the fastest on MI355X).
 int64_t reduce_blocks(int64_t n, int esize)
 {
     const int64_t nv = n * esize / 16;
-    return std::max<int64_t>(1, std::min<int64_t>((nv + 1023) / 1024, 2048));
+    return std::max<int64_t>(1, std::min<int64_t>((nv + 8191) / 8192, 512));
 }
 
 // Workspace pieces of one plan: column partials (nb rows of n), partial dots
@@ -615,9 +617,10 @@ int mep_variant_info(int op, int dtype, int64_t m, int64_t n, int variant, char*
     if (variant < 0 || variant >= cnt)
         return fail(MEP_EINVAL, "variant %d outside 0..%d", variant, cnt - 1);
     const Plan p = plan_stream(es, vec, mode, m, n, variant);
-    snprintf(buf, buf_len, "%s G=%d V=%d B=%d WPE=%d %s threads=%d grid=%lldx%lld",
+    snprintf(buf, buf_len, "%s G=%d V=%d B=%d WPE=%d %s %s threads=%d grid=%lldx%lld",
              vec ? "vec16" : "elem", p.c.G, p.c.V, batch_of(p.c.B, mode), p.c.WPE,
-             p.c.AUX ? "nt" : "cached", p.threads, (long long)p.nb, (long long)p.panels);
+             p.c.AUX ? "nt" : "cached", p.c.MAP ? "blocked" : "cyclic", p.threads, (long long)p.nb,
+             (long long)p.panels);
     return MEP_OK;
 }
 

@@ -13,26 +13,29 @@ namespace mep {
 // Row-group geometry of one streaming-kernel instance: G lanes per row
 // group, V vectors per lane, B rows per batch, WPE waves per SIMD (the
 // register budget is 512 / WPE per lane), AUX the cache-policy bits of the
-// matrix loads (0 = default, 2 = non-temporal streaming).
+// matrix loads (0 = default, 2 = non-temporal streaming).  MAP (a launch
+// argument, not part of the instance) hands row blocks to workgroups
+// cyclically (0) or in contiguous runs (1).
 struct Cfg {
-    int G, V, B, WPE, AUX;
+    int G, V, B, WPE, AUX, MAP = 0;
 };
 
 // Vector path (16-byte loads), ordered by row capacity G * V; among equal
 // capacities the preferred shape comes first (measured on MI355X: streaming
 // the matrix with non-temporal loads is faster for every shape).
-constexpr int kNumVecCfg = 28;
+constexpr int kNumVecCfg = 30;
 constexpr Cfg kVecCfg[kNumVecCfg] = {
     {16, 1, 8, 4, 2},    {16, 1, 8, 4, 0},    {64, 1, 8, 4, 2},    {64, 1, 8, 4, 0},
     {64, 2, 4, 4, 2},    {64, 2, 4, 4, 0},    {64, 4, 2, 4, 2},    {64, 4, 2, 4, 0},
     {256, 2, 4, 4, 2},   {256, 2, 4, 4, 0},   {256, 4, 2, 4, 2},   {256, 4, 2, 4, 0},
     {1024, 2, 4, 4, 2},  {1024, 2, 4, 4, 0},
     // 4096 vectors: a 16384-element fp32 row
-    {512, 8, 2, 2, 2},   {1024, 4, 2, 4, 2},  {512, 8, 1, 4, 2},   {256, 16, 1, 2, 2},
-    {512, 8, 2, 2, 0},   {1024, 4, 2, 4, 0},  {512, 8, 1, 4, 0},   {256, 16, 1, 2, 0},
+    {512, 8, 2, 2, 2},   {512, 8, 2, 2, 2, 1}, {1024, 4, 2, 4, 2},  {512, 8, 1, 4, 2},
+    {256, 16, 1, 2, 2},  {512, 8, 2, 2, 0},    {1024, 4, 2, 4, 0},  {512, 8, 1, 4, 0},
+    {256, 16, 1, 2, 0},
     // 8192 vectors: a 16384-element fp64 row or a 32768-element fp32 row
-    {512, 16, 1, 2, 2},  {1024, 8, 1, 4, 2},  {256, 32, 1, 1, 2},
-    {512, 16, 1, 2, 0},  {1024, 8, 1, 4, 0},  {256, 32, 1, 1, 0}};
+    {512, 16, 1, 2, 2},  {512, 16, 1, 2, 2, 1}, {1024, 8, 1, 4, 2},  {256, 32, 1, 1, 2},
+    {512, 16, 1, 2, 0},  {1024, 8, 1, 4, 0},   {256, 32, 1, 1, 0}};
 // Element-wise path (rows not 16-byte aligned): one element per load.
 constexpr int kNumScalarCfg = 3;
 constexpr Cfg kScalarCfg[kNumScalarCfg] = {{64, 4, 2, 4, 2}, {256, 4, 2, 4, 2}, {1024, 8, 1, 4, 2}};

@@ -60,6 +60,7 @@ struct StreamArgs {
     T* dotpart2;       // multi-panel AXPBY: partial dots of B
     T alpha, beta;
     int64_t m, n, ldp;
+    int blocked;       // row blocks: 0 = block k to workgroup k mod gridDim.x, 1 = contiguous runs
 };
 
 // gfx9-family buffer descriptor, word 3 (raw, untyped 32-bit data).
@@ -105,6 +106,13 @@ template <typename T, int VW>
 __device__ __forceinline__ void store_vec(T* p, typename VecOf<T, VW>::type v)
 {
     *reinterpret_cast<typename VecOf<T, VW>::type*>(p) = v;
+}
+
+// Streaming store: written once, read once by the next kernel.
+template <typename T, int VW>
+__device__ __forceinline__ void store_vec_nt(T* p, typename VecOf<T, VW>::type v)
+{
+    __builtin_nontemporal_store(v, reinterpret_cast<typename VecOf<T, VW>::type*>(p));
 }
 
 // Workgroup barrier that orders LDS traffic only: outstanding global loads
@@ -262,24 +270,13 @@ k_stream(StreamArgs<T> a)
     const vec zero = (vec)(T)0;
 
     vec xv[XLDS ? 1 : V];
-    if constexpr (DOT) {
-        const __amdgpu_buffer_rsrc_t xr = make_rsrc(a.x + col0, pbytes);
-#pragma unroll
-        for (int v = 0; v < V; ++v) {
-            const int64_t c = (int64_t)(v * G + g) * VW;
-            vec t = load_buf<T, VW, 0>(xr, c < PW ? (uint32_t)(c * ES) : kOutOfRange, 0);
-            if constexpr (XLDS)
-                xs[v * THREADS + tid] = t;
-            else
-                xv[v] = t;
-        }
-    }
 
     vec acc[COL ? V : 1];
 #pragma unroll
     for (int v = 0; v < (COL ? V : 1); ++v)
         acc[v] = zero;
 
+    int row_end = m32;  // rows at or past this read as zeros (set before the loop)
     vec ra[B][V], rb[B][V];
     vec sa[TWO ? B : 1][V], sb[TWO ? B : 1][V];
     T wa[WTS ? B : 1], wb[WTS ? B : 1];
@@ -290,7 +287,7 @@ k_stream(StreamArgs<T> a)
         for (int j = 0; j < B; ++j) {
             // first row covered by this wave in batch j, and how many of its rows exist
             const int r0 = blk * BR + j * RG + wgrp0;
-            const int left = m32 - r0;
+            const int left = row_end - r0;
             const int nrows = left < 0 ? 0 : (left < RPW ? left : RPW);
             const uint32_t bytes = WIDE ? (nrows > 0 ? pbytes : 0u) : (uint32_t)(nrows * rowbytes);
             const T* arow = a.A + (int64_t)r0 * n + col0;
@@ -419,30 +416,58 @@ k_stream(StreamArgs<T> a)
 
     // Row blocks blockIdx.x, blockIdx.x + gridDim.x, ...; the trip count is
     // uniform across the workgroup, so the barriers inside are too.
-    // Row blocks blockIdx.x, blockIdx.x + gridDim.x, ...; the trip count is
-    // uniform across the workgroup, so the barriers inside are too.  The next
-    // block is always prefetched: past the last row its resources are empty,
-    // so those loads return zeros without touching memory.  The scheduling
-    // fences keep each refill after the previous use of its buffer, so no
-    // more than two batches are ever live.
+    // Row blocks of this workgroup: blockIdx.x, blockIdx.x + gridDim.x, ...
+    // (cyclic) or one contiguous run (blocked).  The trip count is uniform
+    // across the workgroup, so the barriers inside are too.  The next block
+    // is always prefetched: past the workgroup's last row its resources are
+    // empty, so those loads return zeros without touching memory.  The
+    // scheduling fences keep each refill after the previous use of its
+    // buffer, so no more than two batches are ever live.
     const int nblk = (int)((m + BR - 1) / BR);
-    int blk = blockIdx.x;
-    if (blk < nblk) {
+    int blk, bstep, bend;
+    if (a.blocked) {
+        const int per = (nblk + nbx - 1) / nbx;
+        blk = blockIdx.x * per;
+        bstep = 1;
+        bend = blk + per < nblk ? blk + per : nblk;
+    } else {
+        blk = blockIdx.x;
+        bstep = nbx;
+        bend = nblk;
+    }
+    row_end = bend * BR < m32 ? bend * BR : m32;
+    // the first batch goes out before the dot vector: x comes from L2 (every
+    // workgroup reads the same slice), the matrix from HBM
+    if (blk < bend)
         load_batch(blk, ra, sa, wa);
+    if constexpr (DOT) {
+        const __amdgpu_buffer_rsrc_t xr = make_rsrc(a.x + col0, pbytes);
+#pragma unroll
+        for (int v = 0; v < V; ++v) {
+            const int64_t c = (int64_t)(v * G + g) * VW;
+            vec t = load_buf<T, VW, 0>(xr, c < PW ? (uint32_t)(c * ES) : kOutOfRange, 0);
+            if constexpr (XLDS)
+                xs[v * THREADS + tid] = t;
+            else
+                xv[v] = t;
+        }
+    }
+
+    if (blk < bend) {
         for (;;) {
-            load_batch(blk + nbx, rb, sb, wb);
+            load_batch(blk + bstep, rb, sb, wb);
             __builtin_amdgcn_sched_barrier(0);
             process(blk, 0, ra, sa, wa);
             __builtin_amdgcn_sched_barrier(0);
-            blk += nbx;
-            if (blk >= nblk)
+            blk += bstep;
+            if (blk >= bend)
                 break;
-            load_batch(blk + nbx, ra, sa, wa);
+            load_batch(blk + bstep, ra, sa, wa);
             __builtin_amdgcn_sched_barrier(0);
             process(blk, 1, rb, sb, wb);
             __builtin_amdgcn_sched_barrier(0);
-            blk += nbx;
-            if (blk >= nblk)
+            blk += bstep;
+            if (blk >= bend)
                 break;
         }
     }
@@ -454,7 +479,7 @@ k_stream(StreamArgs<T> a)
             for (int v = 0; v < V; ++v) {
                 const int64_t c = (int64_t)(v * G + g) * VW;
                 if (c < pcols)
-                    store_vec<T, VW>(out + c, acc[v]);
+                    store_vec_nt<T, VW>(out + c, acc[v]);
             }
         } else {
             // row groups of one wave first (butterfly over the lane bits above G) ...
@@ -483,23 +508,27 @@ k_stream(StreamArgs<T> a)
                     t += cred[(w * G + gg) * V + vv];
                 const int64_t c = (int64_t)(vv * G + gg) * VW;
                 if (c < pcols)
-                    store_vec<T, VW>(out + c, t);
+                    store_vec_nt<T, VW>(out + c, t);
             }
         }
     }
 }
 
 // out[j] = sum_{b < nrows} P[b * ldp + j] for j < ncols, rows summed in a fixed
-// order: 16 slices of rows (slice s takes rows s, s + 16, ...), then the slices
-// in ascending order.  With TWO: out = alpha * sum(P) + beta * sum(Q).
-template <typename T, int VW, bool TWO>
-__global__ void __launch_bounds__(256)
+// order: SL = THREADS / 16 slices of rows (slice s takes rows s, s + SL, ...,
+// sixteen of them per step with their loads issued together, missing rows
+// read as zero), then the slices by a fixed pairwise tree in LDS.  With TWO:
+// out = alpha * sum(P) + beta * sum(Q).  Narrow outputs use 1024 threads, so
+// that many partial rows still take one round of loads.
+template <typename T, int VW, bool TWO, int THREADS = 256>
+__global__ void __launch_bounds__(THREADS)
 k_colreduce(const T* __restrict__ P, const T* __restrict__ Q, int64_t ldp, int64_t nrows,
             int64_t ncols, T alpha, T beta, T* __restrict__ out)
 {
     typedef typename VecOf<T, VW>::type vec;
     constexpr int CV = 16;
-    constexpr int SL = 256 / CV;
+    constexpr int SL = THREADS / CV;
+    constexpr int U = 16;
     __shared__ vec rp[SL][CV];
     __shared__ vec rq[TWO ? SL : 1][CV];
     const int tid = threadIdx.x;
@@ -510,17 +539,14 @@ k_colreduce(const T* __restrict__ P, const T* __restrict__ Q, int64_t ldp, int64
     const vec zero = (vec)(T)0;
     vec s = zero, s2 = zero;
     if (ok) {
-        // four rows per step with their loads issued together, still added in
-        // ascending row order
-        constexpr int U = 4;
-        int64_t b = sl;
-        for (; b + (U - 1) * SL < nrows; b += U * SL) {
+        for (int64_t b0 = sl; b0 < nrows; b0 += (int64_t)U * SL) {
             vec t[U], t2[U];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                t[u] = load_vec<T, VW>(P + (b + u * SL) * ldp + col);
+                const int64_t r = b0 + (int64_t)u * SL;
+                t[u] = r < nrows ? load_vec<T, VW>(P + r * ldp + col) : zero;
                 if constexpr (TWO)
-                    t2[u] = load_vec<T, VW>(Q + (b + u * SL) * ldp + col);
+                    t2[u] = r < nrows ? load_vec<T, VW>(Q + r * ldp + col) : zero;
             }
 #pragma unroll
             for (int u = 0; u < U; ++u) {
@@ -529,28 +555,24 @@ k_colreduce(const T* __restrict__ P, const T* __restrict__ Q, int64_t ldp, int64
                     s2 += t2[u];
             }
         }
-        for (; b < nrows; b += SL) {
-            s += load_vec<T, VW>(P + b * ldp + col);
-            if constexpr (TWO)
-                s2 += load_vec<T, VW>(Q + b * ldp + col);
-        }
     }
     rp[sl][cv] = s;
     if constexpr (TWO)
         rq[sl][cv] = s2;
     lds_barrier();
+#pragma unroll
+    for (int stride = SL / 2; stride >= 1; stride >>= 1) {
+        if (sl < stride) {
+            rp[sl][cv] += rp[sl + stride][cv];
+            if constexpr (TWO)
+                rq[sl][cv] += rq[sl + stride][cv];
+        }
+        lds_barrier();
+    }
     if (sl == 0 && ok) {
         vec t = rp[0][cv];
-        vec t2 = zero;
-        if constexpr (TWO)
-            t2 = rq[0][cv];
-#pragma unroll
-        for (int k = 1; k < SL; ++k) {
-            t += rp[k][cv];
-            if constexpr (TWO)
-                t2 += rq[k][cv];
-        }
         if constexpr (TWO) {
+            const vec t2 = rq[0][cv];
 #pragma unroll
             for (int e = 0; e < VW; ++e)
                 t[e] = fma_t(alpha, t[e], beta * t2[e]);
@@ -559,12 +581,13 @@ k_colreduce(const T* __restrict__ P, const T* __restrict__ Q, int64_t ldp, int64
     }
 }
 
-// Sum of a vector, first stage: every workgroup adds a grid-strided share of
-// the 16-byte vectors (four loads in flight per lane, non-temporal), then its
-// lanes (butterfly) and its four waves (ascending) into partial[blockIdx.x].
-// The trailing n mod VW elements are added by the first lanes of workgroup 0.
-// The order depends only on n and gridDim.x, so the result is reproducible;
-// the partials are finished by k_colreduce with one column.
+// Sum of a vector, first stage: workgroup b adds the 16-byte vectors of its
+// own contiguous chunk (lanes stride by 256 vectors, four loads in flight per
+// lane, non-temporal), then its lanes (butterfly) and its four waves
+// (ascending) into partial[b].  The trailing n mod VW elements are added by
+// the first lanes of workgroup 0.  The order depends only on n and
+// gridDim.x, so the result is reproducible; k_colreduce with one column adds
+// the partials.
 template <typename T, int VW>
 __global__ void __launch_bounds__(256)
 k_reduce_sum(const T* __restrict__ x, int64_t n, T* __restrict__ partial)
@@ -573,19 +596,21 @@ k_reduce_sum(const T* __restrict__ x, int64_t n, T* __restrict__ partial)
     constexpr int U = 4;
     const vec* xv = reinterpret_cast<const vec*>(x);
     const int64_t nv = n / VW;
-    const int64_t stride = (int64_t)gridDim.x * 256;
-    int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int64_t chunk = (nv + gridDim.x - 1) / gridDim.x;
+    const int64_t b0 = (int64_t)blockIdx.x * chunk;
+    const int64_t b1 = b0 + chunk < nv ? b0 + chunk : nv;
+    int64_t i = b0 + threadIdx.x;
     vec acc = (vec)(T)0;
-    for (; i + (U - 1) * stride < nv; i += U * stride) {
+    for (; i + (U - 1) * 256 < b1; i += U * 256) {
         vec t[U];
 #pragma unroll
         for (int u = 0; u < U; ++u)
-            t[u] = __builtin_nontemporal_load(xv + i + u * stride);
+            t[u] = __builtin_nontemporal_load(xv + i + u * 256);
 #pragma unroll
         for (int u = 0; u < U; ++u)
             acc += t[u];
     }
-    for (; i < nv; i += stride)
+    for (; i < b1; i += 256)
         acc += __builtin_nontemporal_load(xv + i);
     T s = 0;
 #pragma unroll
@@ -602,8 +627,9 @@ k_reduce_sum(const T* __restrict__ x, int64_t n, T* __restrict__ partial)
         partial[blockIdx.x] = ((red[0] + red[1]) + red[2]) + red[3];
 }
 
-// c = a + b elementwise: grid-strided 16-byte vectors, four in flight per
-// lane, non-temporal loads and stores; the trailing n mod VW elements by
+// c = a + b elementwise: workgroup b handles its own contiguous chunk of
+// 16-byte vectors (lanes stride by 256 vectors, four in flight per lane),
+// with non-temporal loads and stores; the trailing n mod VW elements by
 // workgroup 0.
 template <typename T, int VW>
 __global__ void __launch_bounds__(256)
@@ -615,20 +641,22 @@ k_vector_add(const T* __restrict__ a, const T* __restrict__ b, T* __restrict__ c
     const vec* bv = reinterpret_cast<const vec*>(b);
     vec* cv = reinterpret_cast<vec*>(c);
     const int64_t nv = n / VW;
-    const int64_t stride = (int64_t)gridDim.x * 256;
-    int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    for (; i + (U - 1) * stride < nv; i += U * stride) {
+    const int64_t chunk = (nv + gridDim.x - 1) / gridDim.x;
+    const int64_t b0 = (int64_t)blockIdx.x * chunk;
+    const int64_t b1 = b0 + chunk < nv ? b0 + chunk : nv;
+    int64_t i = b0 + threadIdx.x;
+    for (; i + (U - 1) * 256 < b1; i += U * 256) {
         vec ta[U], tb[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            ta[u] = __builtin_nontemporal_load(av + i + u * stride);
-            tb[u] = __builtin_nontemporal_load(bv + i + u * stride);
+            ta[u] = __builtin_nontemporal_load(av + i + u * 256);
+            tb[u] = __builtin_nontemporal_load(bv + i + u * 256);
         }
 #pragma unroll
         for (int u = 0; u < U; ++u)
-            __builtin_nontemporal_store(ta[u] + tb[u], cv + i + u * stride);
+            __builtin_nontemporal_store(ta[u] + tb[u], cv + i + u * 256);
     }
-    for (; i < nv; i += stride)
+    for (; i < b1; i += 256)
         __builtin_nontemporal_store(__builtin_nontemporal_load(av + i) + __builtin_nontemporal_load(bv + i),
                                     cv + i);
     if (blockIdx.x == 0 && (int64_t)threadIdx.x < n - nv * VW) {
