@@ -11,6 +11,9 @@ Contents
   element summed by one thread in ascending index order.  The paper names these
   kernels (ATAX, BICG, GESUMMV in Tables 1-2, Sec. 4.2) without defining them;
   the textbook definitions are used.
+* ``gemver``: GEMVER (named in Tables 1-2) as the BLAS Technical Forum
+  standard defines it: Ahat = A + u1 v1^T + u2 v2^T, x = beta Ahat^T y + z,
+  w = alpha Ahat x.
 * ``reduce_sum``, ``vector_add``: the sum of a vector and the elementwise sum
   of two vectors (the "reduction" and "vectoradd" samples of Table 3), fp64.
 * ``trimmed_mean``: Eq. 3 of Sec. 3.2 -- sort the R samples ascending, drop the
@@ -69,6 +72,7 @@ class Oracle:
         lib.oracle_reduce_sum.argtypes = [i64, vp]
         lib.oracle_reduce_sum.restype = d
         lib.oracle_vector_add.argtypes = [i64, vp, vp, vp]
+        lib.oracle_gemver.argtypes = [i64, i64, d, d, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
         self.lib = lib
         self.path = lib_path
 
@@ -130,6 +134,22 @@ class Oracle:
         return y
 
 
+    def gemver(self, alpha, beta, A, u1, v1, u2, v2, y, z):
+        """Returns (Ahat, x, w).  alpha, beta are taken as given (pass the
+        element-type values to model an fp32 run)."""
+        A = _f64(A)
+        m, n = self._shape(A)
+        u1, u2, y = _f64(u1), _f64(u2), _f64(y)
+        v1, v2, z = _f64(v1), _f64(v2), _f64(z)
+        assert u1.shape == u2.shape == y.shape == (m,) and v1.shape == v2.shape == z.shape == (n,)
+        Ahat = np.empty((m, n))
+        x = np.empty(n)
+        w = np.empty(m)
+        self.lib.oracle_gemver(m, n, float(alpha), float(beta), A.ctypes.data, u1.ctypes.data,
+                               v1.ctypes.data, u2.ctypes.data, v2.ctypes.data, y.ctypes.data,
+                               z.ctypes.data, Ahat.ctypes.data, x.ctypes.data, w.ctypes.data)
+        return Ahat, x, w
+
     def reduce_sum(self, x) -> float:
         x = _f64(x).ravel()
         return float(self.lib.oracle_reduce_sum(x.size, x.ctypes.data))
@@ -170,6 +190,10 @@ def bicg(A, p, r):
 
 def axpby_mv(alpha, A, beta, B, x):
     return default().axpby_mv(alpha, A, beta, B, x)
+
+
+def gemver(alpha, beta, A, u1, v1, u2, v2, y, z):
+    return default().gemver(alpha, beta, A, u1, v1, u2, v2, y, z)
 
 
 def reduce_sum(x):

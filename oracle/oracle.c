@@ -19,6 +19,10 @@
  * the set of output elements between threads, so the result is bit-identical
  * for any thread count.
  *
+ * GEMVER, which Tables 1-2 also name without a definition, follows the BLAS
+ * Technical Forum standard: Ahat = A + u1 v1^T + u2 v2^T, x = beta Ahat^T y + z,
+ * w = alpha Ahat x.
+ *
  * Two further streaming kernels of the paper's AMD APP SDK table (Table 3,
  * "reduction" and "vectoradd") are defined here too: the sum of a vector and
  * the elementwise sum of two vectors.
@@ -137,4 +141,26 @@ void oracle_vector_add(int64_t n, const double* a, const double* b, double* c)
 #pragma omp parallel for schedule(static)
     for (int64_t i = 0; i < n; ++i)
         c[i] = a[i] + b[i];
+}
+
+/* GEMVER: Ahat_ij = (A_ij + u1_i v1_j) + u2_i v2_j;
+ * x_j = beta * (sum_i Ahat_ij y_i) + z_j  (ascending i);
+ * w_i = alpha * (sum_j Ahat_ij x_j)       (ascending j).
+ * A, Ahat: m x n; u1, u2, y, w: m; v1, v2, z, x: n.  All fp64. */
+void oracle_gemver(int64_t m, int64_t n, double alpha, double beta, const double* A, const double* u1,
+                   const double* v1, const double* u2, const double* v2, const double* y,
+                   const double* z, double* Ahat, double* x, double* w)
+{
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < m; ++i)
+        for (int64_t j = 0; j < n; ++j)
+            Ahat[i * n + j] = (A[i * n + j] + u1[i] * v1[j]) + u2[i] * v2[j];
+    oracle_matvec_t(m, n, Ahat, y, x);
+#pragma omp parallel for schedule(static)
+    for (int64_t j = 0; j < n; ++j)
+        x[j] = beta * x[j] + z[j];
+    oracle_matvec(m, n, Ahat, x, w);
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < m; ++i)
+        w[i] = alpha * w[i];
 }

@@ -299,6 +299,57 @@ def pin_vector_add(orc):
     assert np.array_equal(orc.vector_add(np.arange(5.0), -np.arange(5.0)), np.zeros(5))
 
 
+def _gemver_inputs(m, n, seed, dt, draw=None):
+    draw = draw or datagen.uniform
+    return dict(A=draw(seed, 0, (m, n), dt), u1=draw(seed, 1, (m,), dt), v1=draw(seed, 2, (n,), dt),
+                u2=draw(seed, 3, (m,), dt), v2=draw(seed, 4, (n,), dt), y=draw(seed, 5, (m,), dt),
+                z=draw(seed, 6, (n,), dt))
+
+
+def pin_gemver(orc):
+    """Exact rational GEMVER on small shapes within first-order bounds;
+    integer inputs bit for bit against int64 products; rank-1 closed form."""
+    for (m, n, seed) in ((1, 1, 91), (3, 5, 92), (6, 4, 93), (8, 8, 94)):
+        g = _gemver_inputs(m, n, seed, np.float32)
+        al, be = F(1.5), F(np.float32(1.2))
+        Ah, x, w = orc.gemver(1.5, float(np.float32(1.2)), **g)
+        A = [[F(v) for v in row] for row in g["A"]]
+        E = [[A[i][j] + F(g["u1"][i]) * F(g["v1"][j]) + F(g["u2"][i]) * F(g["v2"][j]) for j in range(n)]
+             for i in range(m)]
+        aE = [[abs(A[i][j]) + abs(F(g["u1"][i]) * F(g["v1"][j])) + abs(F(g["u2"][i]) * F(g["v2"][j]))
+               for j in range(n)] for i in range(m)]
+        for i in range(m):
+            _within(Ah[i], E[i], [gamma(4) * v for v in aE[i]], f"gemver Ahat row {i}")
+        ex = [be * sum((E[i][j] * F(g["y"][i]) for i in range(m)), Fraction(0)) + F(g["z"][j]) for j in range(n)]
+        bx = [gamma(m + 6) * (abs(be) * sum((aE[i][j] * abs(F(g["y"][i])) for i in range(m)), Fraction(0))
+                              + abs(F(g["z"][j]))) for j in range(n)]
+        _within(x, ex, bx, "gemver x")
+        # w uses the oracle's own x: check it against exact arithmetic on that x
+        ew = [al * sum((E[i][j] * F(x[j]) for j in range(n)), Fraction(0)) for i in range(m)]
+        bw = [gamma(n + 6) * abs(al) * sum((aE[i][j] * abs(F(x[j])) for j in range(n)), Fraction(0))
+              for i in range(m)]
+        _within(w, ew, bw, "gemver w")
+    # integer inputs: every value exact in fp64
+    g = _gemver_inputs(120, 90, 95, np.float32, datagen.ternary)
+    Ah, x, w = orc.gemver(2.0, 3.0, **g)
+    I = {k: v.astype(np.int64) for k, v in g.items()}
+    Ei = I["A"] + np.outer(I["u1"], I["v1"]) + np.outer(I["u2"], I["v2"])
+    xi = 3 * (Ei.T @ I["y"]) + I["z"]
+    wi = 2 * (Ei @ xi)
+    assert np.array_equal(Ah, Ei.astype(np.float64)) and np.array_equal(x, xi.astype(np.float64))
+    assert np.array_equal(w, wi.astype(np.float64)), "integer gemver"
+    # A = 0, u2 = 0: Ahat = u1 v1^T, x = beta (u1.y) v1 + z, w = alpha (v1.x) u1; dyadic values make it exact
+    m, n = 7, 9
+    u1 = np.arange(1, m + 1, dtype=np.float64) / 4
+    v1 = np.arange(-4, n - 4, dtype=np.float64) / 2
+    y = np.ones(m)
+    z = np.full(n, 0.5)
+    Ah, x, w = orc.gemver(0.5, 2.0, np.zeros((m, n)), u1, v1, np.zeros(m), np.zeros(n), y, z)
+    assert np.array_equal(Ah, np.outer(u1, v1))
+    assert np.array_equal(x, 2.0 * u1.sum() * v1 + z)
+    assert np.array_equal(w, 0.5 * float(v1 @ x) * u1)
+
+
 ALL_PINS = [
     pin_bruteforce_matvec,
     pin_bruteforce_matvec_t,
@@ -312,4 +363,5 @@ ALL_PINS = [
     pin_numpy_crosscheck,
     pin_reduce_sum,
     pin_vector_add,
+    pin_gemver,
 ]

@@ -39,6 +39,11 @@ MUTANTS = {
                            "for (int64_t i = 1; i < n; ++i)\n        s += x[i];"),
     "reduce_fp32_accumulator": ("double s = 0.0;", "float s = 0.0f;"),
     "vector_add_subtracts": ("c[i] = a[i] + b[i];", "c[i] = a[i] - b[i];"),
+    "gemver_drops_second_update": ("Ahat[i * n + j] = (A[i * n + j] + u1[i] * v1[j]) + u2[i] * v2[j];",
+                                   "Ahat[i * n + j] = A[i * n + j] + u1[i] * v1[j];"),
+    "gemver_w_from_A": ("oracle_matvec(m, n, Ahat, x, w);", "oracle_matvec(m, n, A, x, w);"),
+    "gemver_x_misses_z": ("x[j] = beta * x[j] + z[j];", "x[j] = beta * x[j];"),
+    "gemver_swapped_scalars": ("w[i] = alpha * w[i];", "w[i] = beta * w[i];"),
 }
 
 RUNNER = r"""
