@@ -67,7 +67,8 @@ enum {
     MEP_OP_ATA_X = 3,    /* y = A^T (A x) (ATAX)                             */
     MEP_OP_AXPBY_MV = 4, /* y = alpha A x + beta B x (GESUMMV)               */
     MEP_OP_REDUCE_SUM = 5, /* s = sum_i x_i ("reduction", Table 3); m = 1    */
-    MEP_OP_VECTOR_ADD = 6  /* c = a + b ("vectoradd", Table 3); m = 1        */
+    MEP_OP_VECTOR_ADD = 6, /* c = a + b ("vectoradd", Table 3); m = 1        */
+    MEP_OP_GEMVER = 7      /* GEMVER (Tables 1-2), see mep_gemver            */
 };
 
 typedef void* mep_stream_t; /* hipStream_t */
@@ -110,6 +111,21 @@ int mep_axpby_mv(int dtype, int64_t m, int64_t n, double alpha, const void* A, d
                  mep_stream_t stream);
 
 /*
+ * GEMVER (named in Tables 1-2; the paper gives no definition, this is the BLAS
+ * Technical Forum standard's):
+ *     Ahat = A + u1 v1^T + u2 v2^T,   x = beta Ahat^T y + z,   w = alpha Ahat x.
+ * A, Ahat: m x n; u1, u2, y, w: m; v1, v2, z, x: n.  Ahat may be A itself (the
+ * in-place update of the standard); no other overlap is allowed.  Two passes
+ * over the matrix: the first reads A, forms and stores Ahat and accumulates
+ * Ahat^T y in the same pass; the second reads Ahat for w (it needs the whole
+ * x).  On the fp32 path alpha and beta are rounded to fp32.  Workspace:
+ * mep_workspace_bytes(MEP_OP_GEMVER, dtype, m, n).
+ */
+int mep_gemver(int dtype, int64_t m, int64_t n, double alpha, double beta, const void* A, void* Ahat,
+               const void* u1, const void* v1, const void* u2, const void* v2, const void* y,
+               const void* z, void* x, void* w, void* ws, size_t ws_bytes, mep_stream_t stream);
+
+/*
  * s = sum_{i<n} x_i: the "reduction" sample of the AMD APP SDK table (Table 3,
  * Sec. 4.3).  x: n elements; s: one element of device memory.  Workgroups add
  * grid-strided shares into partials in ws (mep_workspace_bytes(
@@ -136,6 +152,8 @@ int mep_vector_add(int dtype, int64_t n, const void* a, const void* b, void* c,
  *   AXPBY_MV  A, B, in0 = x, out0 = y, alpha, beta
  *   REDUCE_SUM  in0 = x, out0 = s (m = 1, n = length)
  *   VECTOR_ADD  in0 = a, in1 = b, out0 = c (m = 1, n = length)
+ *   GEMVER    A, in0..in5 = u1, v1, u2, v2, y, z, out0 = x, out1 = w,
+ *             out2 = Ahat, alpha, beta
  * flush_buf / flush_bytes: optional device buffer the harness overwrites
  * before every timed sample so that no operand stays in the caches.
  */
@@ -155,6 +173,11 @@ typedef struct {
     mep_stream_t stream;
     void* flush_buf;
     size_t flush_bytes;
+    const void* in2;
+    const void* in3;
+    const void* in4;
+    const void* in5;
+    void* out2;
 } mep_call_t;
 
 /* Runs one call as described above (the same checks, the same kernels). */
@@ -220,7 +243,9 @@ int mep_variant_info(int op, int dtype, int64_t m, int64_t n, int variant, char*
  * apply != 0 the winner becomes the op's variant (mep_set_variant), else the
  * previous setting is restored.  results (nullable, results_cap entries)
  * receives, per candidate, the trimmed mean (ms; NaN when not timed), the FE
- * error against the baseline and the FE verdict.  The candidate set is fixed,
+ * error against the baseline (each output on its own scale, the worse of
+ * the two) and the FE verdict.  A GEMVER call must be out of place (out2 !=
+ * A), else MEP_EINVAL: each in-place run changes A.  The candidate set is fixed,
  * so one round is the whole search (the paper's D rounds regenerate
  * candidates; here nothing new appears in a later round).  Synchronizes
  * call->stream; overwrites the call's outputs.
@@ -247,6 +272,10 @@ int mep_select_variant(const mep_call_t* call, int warmup, int R, int k, int inn
  */
 int mep_profile_begin(int capacity);
 int mep_profile_end(double* total_ms, int* launches);
+/* As mep_profile_end, but also returns each recorded launch's duration in
+ * launch order (up to cap entries; operations with two streaming passes, such
+ * as GEMVER, record two launches per call). */
+int mep_profile_end_samples(double* samples_ms, int cap, double* total_ms, int* launches);
 
 /*
  * Plain device copy of `bytes` bytes (16-byte vector loads and stores):

@@ -66,6 +66,9 @@ static Cfg preferred_shape(int mode, int esize, int64_t m, int64_t n, int64_t nv
         return Cfg{64, 1, 8, 4, aux};
     if (nv <= 256)
         return Cfg{64, 4, 2, 4, aux};
+    // the rank-2 update that stores Ahat: 1024-lane groups (panels past 4096 vectors)
+    if (mode & F_STORE)
+        return Cfg{1024, 4, 2, 4, aux};
     if (nv <= 4096)
         return Cfg{512, 8, 2, 2, aux};
     return Cfg{512, 16, 1, 2, aux};
@@ -145,7 +148,7 @@ Plan plan_stream(int esize, bool vec, int mode, int64_t m, int64_t n, int varian
     return p;
 }
 
-static std::atomic<int> g_variant[7] = {{-1}, {-1}, {-1}, {-1}, {-1}, {-1}, {-1}};
+static std::atomic<int> g_variant[8] = {{-1}, {-1}, {-1}, {-1}, {-1}, {-1}, {-1}, {-1}};
 
 static int op_mode(int op)
 {
@@ -155,6 +158,7 @@ static int op_mode(int op)
     case MEP_OP_BICG: return MODE_BICG;
     case MEP_OP_ATA_X: return MODE_ATAX;
     case MEP_OP_AXPBY_MV: return MODE_AXPBY;
+    case MEP_OP_GEMVER: return MODE_GEMV1;
     default: return -1;
     }
 }
@@ -212,7 +216,16 @@ static size_t ws_bytes_mode(int mode, int esize, int64_t m, int64_t n)
         const int cnt = stream_candidates(esize, vec, mode, m, n, idx);
         for (int k = 0; k < cnt; ++k) {
             const Plan p = plan_stream(esize, vec, mode, m, n, k);
-            if (mode == MODE_ATAX && p.panels > 1) {
+            if (mode == MODE_GEMV1) {
+                // pass 1 column partials, then (reusing the space) pass 2 partial dots
+                size_t s2 = 0;
+                int i2[16];
+                const int c2 = stream_candidates(esize, vec, MODE_MV, m, n, i2);
+                for (int k2 = 0; k2 < c2; ++k2)
+                    s2 = std::max(s2, layout_for(MODE_MV, plan_stream(esize, vec, MODE_MV, m, n, k2), esize,
+                                                 m, n, false).total);
+                best = std::max(best, std::max(layout_for(mode, p, esize, m, n, false).total, s2));
+            } else if (mode == MODE_ATAX && p.panels > 1) {
                 // two passes: A x over panels, then A^T t over panels
                 size_t s = 0;
                 for (int k2 = 0; k2 < 16; ++k2) {
@@ -373,7 +386,7 @@ static int run_matvec(int64_t m, int64_t n, const T* A, const T* x, T* y, char* 
         a.dotpart = reinterpret_cast<T*>(ws);
         e = stream_launch<T>(p, MODE_MV, a, s);
         if (e == hipSuccess)
-            e = launch_colreduce<T>(a.dotpart, nullptr, m, p.panels, m, (T)1, (T)0, y, s);
+            e = launch_colreduce<T>(a.dotpart, nullptr, m, p.panels, m, (T)1, (T)0, y, s, EPI_SCALE);
     }
     return e == hipSuccess ? MEP_OK : hip_fail(e, "matvec launch");
 }
@@ -410,9 +423,9 @@ static int run_matvec_t(int64_t m, int64_t n, const T* A, const T* w, T* z, cons
     }
     e = stream_launch<T>(p, mode, a, s);
     if (e == hipSuccess)
-        e = launch_colreduce<T>(a.colpart, nullptr, n, p.nb, n, (T)1, (T)0, z, s);
+        e = launch_colreduce<T>(a.colpart, nullptr, n, p.nb, n, (T)1, (T)0, z, s, EPI_SCALE);
     if (e == hipSuccess && pair && p.panels > 1)
-        e = launch_colreduce<T>(a.dotpart, nullptr, m, p.panels, m, (T)1, (T)0, q, s);
+        e = launch_colreduce<T>(a.dotpart, nullptr, m, p.panels, m, (T)1, (T)0, q, s, EPI_SCALE);
     return e == hipSuccess ? MEP_OK : hip_fail(e, "matvec_t launch");
 }
 
@@ -440,7 +453,7 @@ static int run_ata_x(int64_t m, int64_t n, const T* A, const T* x, T* y, T* t, c
         a.colpart = reinterpret_cast<T*>(ws);
         e = stream_launch<T>(p, MODE_ATAX, a, s);
         if (e == hipSuccess)
-            e = launch_colreduce<T>(a.colpart, nullptr, n, p.nb, n, (T)1, (T)0, y, s);
+            e = launch_colreduce<T>(a.colpart, nullptr, n, p.nb, n, (T)1, (T)0, y, s, EPI_SCALE);
         return e == hipSuccess ? MEP_OK : hip_fail(e, "ata_x launch");
     }
     // rows too long to keep on chip: t = A x over column panels, then A^T t
@@ -458,7 +471,7 @@ static int run_ata_x(int64_t m, int64_t n, const T* A, const T* x, T* y, T* t, c
         a1.rowout = tt;
     e = stream_launch<T>(p1, MODE_MV, a1, s);
     if (e == hipSuccess && p1.panels > 1)
-        e = launch_colreduce<T>(dot, nullptr, m, p1.panels, m, (T)1, (T)0, tt, s);
+        e = launch_colreduce<T>(dot, nullptr, m, p1.panels, m, (T)1, (T)0, tt, s, EPI_SCALE);
     if (e == hipSuccess) {
         StreamArgs<T> a2 = empty_args<T>(m, n);
         a2.A = A;
@@ -466,7 +479,7 @@ static int run_ata_x(int64_t m, int64_t n, const T* A, const T* x, T* y, T* t, c
         a2.colpart = colpart;
         e = stream_launch<T>(p2, MODE_ATW, a2, s);
         if (e == hipSuccess)
-            e = launch_colreduce<T>(colpart, nullptr, n, p2.nb, n, (T)1, (T)0, y, s);
+            e = launch_colreduce<T>(colpart, nullptr, n, p2.nb, n, (T)1, (T)0, y, s, EPI_SCALE);
     }
     return e == hipSuccess ? MEP_OK : hip_fail(e, "ata_x launch");
 }
@@ -499,7 +512,7 @@ static int run_axpby(int64_t m, int64_t n, T alpha, const T* A, T beta, const T*
         a.dotpart2 = reinterpret_cast<T*>(ws + l.dotpart);
         e = stream_launch<T>(p, MODE_AXPBY, a, s);
         if (e == hipSuccess)
-            e = launch_colreduce<T>(a.dotpart, a.dotpart2, m, p.panels, m, alpha, beta, y, s);
+            e = launch_colreduce<T>(a.dotpart, a.dotpart2, m, p.panels, m, alpha, beta, y, s, EPI_TWO);
     }
     return e == hipSuccess ? MEP_OK : hip_fail(e, "axpby_mv launch");
 }
@@ -551,6 +564,59 @@ hipError_t launch_flush(void* buf, size_t bytes, uint32_t tag, hipStream_t s)
     const int64_t blocks = std::min<int64_t>((count + 255) / 256, 256 * 16);
     hipLaunchKernelGGL(k_flush16, dim3((unsigned)blocks), dim3(256), 0, s, (uint4*)buf, count, tag);
     return hipGetLastError();
+}
+
+template <typename T>
+static int run_gemver(int64_t m, int64_t n, T alpha, T beta, const T* A, T* Ahat, const T* u1, const T* v1,
+                      const T* u2, const T* v2, const T* y, const T* z, T* x, T* w, char* ws, hipStream_t s)
+{
+    hipError_t e = hipSuccess;
+    if (n == 0) {
+        e = launch_fill_zero<T>(w, m, s);
+        return e == hipSuccess ? MEP_OK : hip_fail(e, "fill");
+    }
+    if (m == 0) {
+        // x = beta * (empty sum) + z
+        e = launch_colreduce<T>(reinterpret_cast<const T*>(z), z, n, 0, n, beta, (T)0, x, s, EPI_ADDVEC);
+        return e == hipSuccess ? MEP_OK : hip_fail(e, "gemver launch");
+    }
+    // pass 1: Ahat = A + u1 v1^T + u2 v2^T, stored; column partials of Ahat^T y
+    const bool vec1 = vec_ok_n(sizeof(T), n) && aligned(A, 16) && aligned(Ahat, 16) && aligned(v1, 16) &&
+                      aligned(v2, 16);
+    const Plan p1 = plan_stream(sizeof(T), vec1, MODE_GEMV1, m, n, variant_of(MEP_OP_GEMVER));
+    StreamArgs<T> a1 = empty_args<T>(m, n);
+    a1.A = A;
+    a1.Aout = Ahat;
+    a1.w = y;
+    a1.u1 = u1;
+    a1.u2 = u2;
+    a1.v1 = v1;
+    a1.v2 = v2;
+    a1.colpart = reinterpret_cast<T*>(ws);
+    e = stream_launch<T>(p1, MODE_GEMV1, a1, s);
+    // x = beta * (Ahat^T y) + z
+    if (e == hipSuccess)
+        e = launch_colreduce<T>(a1.colpart, z, n, p1.nb, n, beta, (T)0, x, s, EPI_ADDVEC);
+    // pass 2: w = alpha * Ahat x
+    if (e == hipSuccess) {
+        const bool vec2 = vec_ok_n(sizeof(T), n) && aligned(Ahat, 16) && aligned(x, 16);
+        const Plan p2 = plan_stream(sizeof(T), vec2, MODE_MV, m, n, -1);
+        StreamArgs<T> a2 = empty_args<T>(m, n);
+        a2.A = Ahat;
+        a2.x = x;
+        a2.alpha = alpha;
+        a2.scale_rows = 1;
+        if (p2.panels == 1) {
+            a2.rowout = w;
+            e = stream_launch<T>(p2, MODE_MV, a2, s);
+        } else {
+            a2.dotpart = reinterpret_cast<T*>(ws);
+            e = stream_launch<T>(p2, MODE_MV, a2, s);
+            if (e == hipSuccess)
+                e = launch_colreduce<T>(a2.dotpart, nullptr, m, p2.panels, m, alpha, (T)0, w, s, EPI_SCALE);
+        }
+    }
+    return e == hipSuccess ? MEP_OK : hip_fail(e, "gemver launch");
 }
 
 }  // namespace mep
@@ -742,6 +808,47 @@ int mep_axpby_mv(int dtype, int64_t m, int64_t n, double alpha, const void* A, d
                              (double*)y, (char*)ws, s);
 }
 
+int mep_gemver(int dtype, int64_t m, int64_t n, double alpha, double beta, const void* A, void* Ahat,
+               const void* u1, const void* v1, const void* u2, const void* v2, const void* y, const void* z,
+               void* x, void* w, void* ws, size_t ws_bytes, mep_stream_t stream)
+{
+    int rc = check_sizes(dtype, m, n);
+    if (rc)
+        return rc;
+    const int es = esize_of(dtype);
+    if ((rc = check_ptr(A, m * n, es, "A")) || (rc = check_ptr(Ahat, m * n, es, "Ahat")) ||
+        (rc = check_ptr(u1, m, es, "u1")) || (rc = check_ptr(v1, n, es, "v1")) ||
+        (rc = check_ptr(u2, m, es, "u2")) || (rc = check_ptr(v2, n, es, "v2")) ||
+        (rc = check_ptr(y, m, es, "y")) || (rc = check_ptr(z, n, es, "z")) || (rc = check_ptr(x, n, es, "x")) ||
+        (rc = check_ptr(w, m, es, "w")))
+        return rc;
+    const size_t need = mep_workspace_bytes(MEP_OP_GEMVER, dtype, m, n);
+    if ((rc = check_ws(ws, ws_bytes, need)))
+        return rc;
+    const size_t mat = (size_t)(m * n) * es;
+    // Ahat may be A itself (in-place update); otherwise it must not overlap A
+    const Range aRange{Ahat == A ? nullptr : A, mat, "A"};
+    const Range outs[] = {{Ahat, mat, "Ahat"}, {x, (size_t)n * es, "x"}, {w, (size_t)m * es, "w"}};
+    const Range ins[] = {aRange,
+                         {u1, (size_t)m * es, "u1"},
+                         {v1, (size_t)n * es, "v1"},
+                         {u2, (size_t)m * es, "u2"},
+                         {v2, (size_t)n * es, "v2"},
+                         {y, (size_t)m * es, "y"},
+                         {z, (size_t)n * es, "z"},
+                         {ws, need, "ws"}};
+    if ((rc = check_overlaps(outs, 3, ins, 8)))
+        return rc;
+    hipStream_t s = (hipStream_t)stream;
+    if (dtype == MEP_F32)
+        return run_gemver<float>(m, n, (float)alpha, (float)beta, (const float*)A, (float*)Ahat, (const float*)u1,
+                                 (const float*)v1, (const float*)u2, (const float*)v2, (const float*)y,
+                                 (const float*)z, (float*)x, (float*)w, (char*)ws, s);
+    return run_gemver<double>(m, n, alpha, beta, (const double*)A, (double*)Ahat, (const double*)u1,
+                              (const double*)v1, (const double*)u2, (const double*)v2, (const double*)y,
+                              (const double*)z, (double*)x, (double*)w, (char*)ws, s);
+}
+
 int mep_reduce_sum(int dtype, int64_t n, const void* x, void* out, void* ws, size_t ws_bytes,
                    mep_stream_t stream)
 {
@@ -817,6 +924,9 @@ int mep_run(const mep_call_t* c)
         return mep_reduce_sum(c->dtype, c->n, c->in0, c->out0, c->ws, c->ws_bytes, c->stream);
     case MEP_OP_VECTOR_ADD:
         return mep_vector_add(c->dtype, c->n, c->in0, c->in1, c->out0, c->stream);
+    case MEP_OP_GEMVER:
+        return mep_gemver(c->dtype, c->m, c->n, c->alpha, c->beta, c->A, c->out2, c->in0, c->in1, c->in2,
+                          c->in3, c->in4, c->in5, c->out0, c->out1, c->ws, c->ws_bytes, c->stream);
     default:
         return fail(MEP_EINVAL, "unknown op %d", c->op);
     }
@@ -899,6 +1009,7 @@ static void output_lengths(const mep_call_t* c, int64_t* l0, int64_t* l1)
     case MEP_OP_AXPBY_MV: *l0 = c->m; break;
     case MEP_OP_REDUCE_SUM: *l0 = 1; break;
     case MEP_OP_VECTOR_ADD: *l0 = c->n; break;
+    case MEP_OP_GEMVER: *l0 = c->n; *l1 = c->m; break;
     default: *l0 = 0; break;
     }
 }
@@ -928,11 +1039,11 @@ static int run_and_fetch(const mep_call_t* c, std::vector<double>& out)
     return MEP_OK;
 }
 
-// The FE metric of mep_check_fe on two host fp64 vectors.
-static double fe_metric(const std::vector<double>& out, const std::vector<double>& ref)
+// The FE metric of mep_check_fe on elements [lo, hi) of two host fp64 vectors.
+static double fe_metric(const std::vector<double>& out, const std::vector<double>& ref, size_t lo, size_t hi)
 {
     double worst = 0.0, scale = 0.0;
-    for (size_t i = 0; i < out.size(); ++i) {
+    for (size_t i = lo; i < hi; ++i) {
         if (!std::isfinite(out[i]))
             return std::numeric_limits<double>::infinity();
         scale = std::max(scale, std::fabs(ref[i]));
@@ -941,6 +1052,14 @@ static double fe_metric(const std::vector<double>& out, const std::vector<double
     if (scale == 0.0)
         return worst == 0.0 ? 0.0 : std::numeric_limits<double>::infinity();
     return worst / scale;
+}
+
+// Each output of a call is judged on its own scale; the worse one counts.
+static double fe_metric_call(const mep_call_t* c, const std::vector<double>& out, const std::vector<double>& ref)
+{
+    int64_t l0, l1;
+    output_lengths(c, &l0, &l1);
+    return std::max(fe_metric(out, ref, 0, (size_t)l0), fe_metric(out, ref, (size_t)l0, (size_t)(l0 + l1)));
 }
 
 int mep_select_variant(const mep_call_t* call, int warmup, int R, int k, int inner, int flush, double tol,
@@ -952,6 +1071,8 @@ int mep_select_variant(const mep_call_t* call, int warmup, int R, int k, int inn
         return fail(MEP_EINVAL, "unknown op %d", call->op);
     if (k < 0 || R <= 2 * k || inner < 1 || warmup < 0)
         return fail(MEP_EBUDGET, "Eq. 3 needs R > 2k >= 0, inner >= 1, warmup >= 0");
+    if (call->op == MEP_OP_GEMVER && call->out2 == call->A && call->A != nullptr)
+        return fail(MEP_EINVAL, "selection needs an out-of-place GEMVER call (each in-place run changes A)");
     const int count = mep_variant_count(call->op, call->dtype, call->m, call->n);
     if (count < 1)
         return fail(MEP_EINVAL, "no candidates for this call");
@@ -966,7 +1087,7 @@ int mep_select_variant(const mep_call_t* call, int warmup, int R, int k, int inn
         rc = run_and_fetch(call, v == 0 ? base : out);
         if (rc)
             break;
-        r.fe_err = v == 0 ? 0.0 : fe_metric(out, base);
+        r.fe_err = v == 0 ? 0.0 : fe_metric_call(call, out, base);
         r.fe_pass = r.fe_err <= tol ? 1 : 0;
         if (r.fe_pass) {
             rc = mep_time_trimmed(call, warmup, R, k, inner, flush, &r.mean_ms, nullptr);
@@ -1048,8 +1169,15 @@ int mep_profile_begin(int capacity)
 
 int mep_profile_end(double* total_ms, int* launches)
 {
+    return mep_profile_end_samples(nullptr, 0, total_ms, launches);
+}
+
+int mep_profile_end_samples(double* samples_ms, int cap, double* total_ms, int* launches)
+{
     if (!g_prof.armed)
         return fail(MEP_EINVAL, "profiling is not armed");
+    if (cap < 0 || (samples_ms == nullptr && cap > 0))
+        return fail(MEP_EINVAL, "bad sample buffer");
     double tot = 0.0;
     hipError_t e = hipSuccess;
     for (int i = 0; i < g_prof.used && e == hipSuccess; ++i) {
@@ -1058,6 +1186,8 @@ int mep_profile_end(double* total_ms, int* launches)
         if (e == hipSuccess)
             e = hipEventElapsedTime(&ms, g_prof.start[i], g_prof.stop[i]);
         tot += ms;
+        if (samples_ms != nullptr && i < cap)
+            samples_ms[i] = ms;
     }
     const int used = g_prof.used;
     for (hipEvent_t x : g_prof.start)

@@ -45,20 +45,35 @@ constexpr Cfg kScalarCfg[kNumScalarCfg] = {{64, 4, 2, 4, 2}, {256, 4, 2, 4, 2}, 
 constexpr int batch_of(int B, int mode) { return (mode & F_TWO) ? (B > 1 ? B / 2 : 1) : B; }
 
 // Rough per-lane register need of an instance (vgpr32 = registers per
-// loaded vector): two row buffers, the column sums, the register copy of
-// the dot vector and some fixed overhead.  Instances above the budget of
+// loaded vector): two row buffers, the column sums, the register copies of
+// the column vectors, the rank-2 row scalars and some fixed overhead.  Instances above the budget of
 // their occupancy target are never built or chosen.
+constexpr int n_colvecs(int mode) { return ((mode & F_DOT) ? 1 : 0) + ((mode & F_RANK2) ? 2 : 0); }
+constexpr bool colvecs_in_lds(Cfg c, int mode, int vgpr32)
+{
+    return n_colvecs(mode) > 0 && n_colvecs(mode) * c.V * vgpr32 * 4 > (c.WPE <= 2 ? 128 : 64);
+}
 constexpr int vgpr_estimate(Cfg c, int mode, int vgpr32)
 {
     const int mats = (mode & F_TWO) ? 2 : 1;
     const int bufs = 2 * mats * batch_of(c.B, mode) * c.V * vgpr32;
     const int col = (mode & F_COL) ? c.V * vgpr32 : 0;
-    const int xbytes = c.V * vgpr32 * 4;
-    const bool xlds = (mode & F_DOT) && xbytes > (c.WPE <= 2 ? 128 : 64);
-    const int x = ((mode & F_DOT) && !xlds) ? c.V * vgpr32 : 0;
-    return bufs + col + x + 24;
+    const int x = colvecs_in_lds(c, mode, vgpr32) ? 0 : n_colvecs(mode) * c.V * vgpr32;
+    // rank-2 update: u1 and u2 of every row of both batches (two registers
+    // each for fp64) and the store addressing
+    const int u = (mode & F_RANK2) ? 8 * batch_of(c.B, mode) + 8 : 0;
+    return bufs + col + x + u + 24;
 }
-constexpr bool cfg_fits(Cfg c, int mode, int vgpr32) { return vgpr_estimate(c, mode, vgpr32) <= 512 / c.WPE; }
+// LDS of the per-lane column-vector slots (the other arrays are small).
+constexpr int lds_estimate(Cfg c, int mode, int vgpr32)
+{
+    const int threads = c.G < 256 ? 256 : c.G;
+    return colvecs_in_lds(c, mode, vgpr32) ? n_colvecs(mode) * c.V * threads * vgpr32 * 4 : 0;
+}
+constexpr bool cfg_fits(Cfg c, int mode, int vgpr32)
+{
+    return vgpr_estimate(c, mode, vgpr32) <= 512 / c.WPE && lds_estimate(c, mode, vgpr32) <= 144 * 1024;
+}
 
 struct Plan {
     bool vec;         // 16-byte vector path
@@ -89,7 +104,7 @@ hipError_t launch_stream(const Plan& p, int mode, const StreamArgs<T>& a, hipStr
 
 template <typename T>
 hipError_t launch_colreduce(const T* P, const T* Q, int64_t ldp, int64_t nrows, int64_t ncols,
-                            T alpha, T beta, T* out, hipStream_t s);
+                            T alpha, T beta, T* out, hipStream_t s, int epi);
 
 template <typename T>
 hipError_t launch_fill_zero(T* p, int64_t count, hipStream_t s);
@@ -101,10 +116,10 @@ template <>
 hipError_t launch_stream<double>(const Plan&, int, const StreamArgs<double>&, hipStream_t, const LaunchEvents&);
 template <>
 hipError_t launch_colreduce<float>(const float*, const float*, int64_t, int64_t, int64_t, float, float,
-                                   float*, hipStream_t);
+                                   float*, hipStream_t, int);
 template <>
 hipError_t launch_colreduce<double>(const double*, const double*, int64_t, int64_t, int64_t, double,
-                                    double, double*, hipStream_t);
+                                    double, double*, hipStream_t, int);
 template <>
 hipError_t launch_fill_zero<float>(float*, int64_t, hipStream_t);
 template <>

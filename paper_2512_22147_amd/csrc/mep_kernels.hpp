@@ -34,13 +34,14 @@
 
 namespace mep {
 
-enum : int { F_DOT = 1, F_TWO = 2, F_COL = 4, F_FROMDOT = 8 };
+enum : int { F_DOT = 1, F_TWO = 2, F_COL = 4, F_FROMDOT = 8, F_RANK2 = 16, F_STORE = 32 };
 enum : int {
-    MODE_MV = F_DOT,                         // y = A x
+    MODE_MV = F_DOT,                         // y = A x (optionally scaled by alpha)
     MODE_AXPBY = F_DOT | F_TWO,              // y = alpha A x + beta B x
     MODE_ATW = F_COL,                        // z = A^T w
     MODE_BICG = F_DOT | F_COL,               // q = A p, s = A^T r
-    MODE_ATAX = F_DOT | F_COL | F_FROMDOT    // y = A^T (A x)
+    MODE_ATAX = F_DOT | F_COL | F_FROMDOT,   // y = A^T (A x)
+    MODE_GEMV1 = F_COL | F_RANK2 | F_STORE   // Ahat = A + u1 v1^T + u2 v2^T stored, and Ahat^T y
 };
 
 template <typename T, int VW>
@@ -58,9 +59,15 @@ struct StreamArgs {
     T* colpart;        // column partials P[gridDim.x][ldp]
     T* dotpart;        // multi-panel: partial dots D[panel][m]
     T* dotpart2;       // multi-panel AXPBY: partial dots of B
+    const T* u1;       // rank-2 update (GEMVER): row factors, length m
+    const T* u2;
+    const T* v1;       // ... and column factors, length n
+    const T* v2;
+    T* Aout;           // the updated matrix (may equal A)
     T alpha, beta;
     int64_t m, n, ldp;
     int blocked;       // row blocks: 0 = block k to workgroup k mod gridDim.x, 1 = contiguous runs
+    int scale_rows;    // MV: rowout = alpha * dot instead of dot
 };
 
 // gfx9-family buffer descriptor, word 3 (raw, untyped 32-bit data).
@@ -94,6 +101,23 @@ load_buf(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff)
         return __builtin_bit_cast(vec, __builtin_amdgcn_raw_buffer_load_b64(r, (int)voff, (int)soff, AUX));
     else
         return __builtin_bit_cast(vec, __builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)soff, AUX));
+}
+
+// 4, 8 or 16-byte raw buffer store; stores of out-of-range lanes are dropped.
+template <typename T, int VW, int AUX>
+__device__ __forceinline__ void store_buf(typename VecOf<T, VW>::type v, __amdgpu_buffer_rsrc_t r,
+                                          uint32_t voff)
+{
+    typedef typename VecOf<T, VW>::type vec;
+    if constexpr (sizeof(vec) == 16) {
+        typedef unsigned int u4 __attribute__((ext_vector_type(4)));
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u4, v), r, (int)voff, 0, AUX);
+    } else if constexpr (sizeof(vec) == 8) {
+        typedef unsigned int u2 __attribute__((ext_vector_type(2)));
+        __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u2, v), r, (int)voff, 0, AUX);
+    } else {
+        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned int, v), r, (int)voff, 0, AUX);
+    }
 }
 
 template <typename T, int VW>
@@ -210,12 +234,16 @@ k_stream(StreamArgs<T> a)
     constexpr bool COL = (MODE & F_COL) != 0;
     constexpr bool FROMDOT = (MODE & F_FROMDOT) != 0;
     constexpr bool WTS = COL && !FROMDOT;
-    // the dot vector lives in registers when its slice is small against the
-    // register budget (512 / WPE per lane), else in per-lane LDS slots
-    constexpr bool XLDS = DOT && (V * VB > (WPE <= 2 ? 128u : 64u));
+    constexpr bool RANK2 = (MODE & F_RANK2) != 0;
+    constexpr bool STORE = (MODE & F_STORE) != 0;
+    // the column vectors each lane keeps (x; or v1 and v2) live in registers
+    // when their slices are small against the register budget (512 / WPE per
+    // lane), else in per-lane LDS slots
+    constexpr int NXV = (DOT ? 1 : 0) + (RANK2 ? 2 : 0);
+    constexpr bool XLDS = NXV > 0 && (NXV * V * VB > (WPE <= 2 ? 128u : 64u));
     constexpr int NDOT = TWO ? 2 : 1;
 
-    __shared__ vec xs[XLDS ? V * THREADS : 1];
+    __shared__ vec xs[XLDS ? NXV * V * THREADS : 1];
     __shared__ T red[2][(G > 64) ? NDOT * B * WPG : 1];
     __shared__ vec cred[(COL && RG > 1) ? NWAVES * G * V : 1];
 
@@ -269,7 +297,14 @@ k_stream(StreamArgs<T> a)
 
     const vec zero = (vec)(T)0;
 
-    vec xv[XLDS ? 1 : V];
+    vec xv[XLDS ? 1 : NXV * V + 1];
+    // slot k (0: x or v1, 1: v2) of vector v
+    auto colvec = [&](int k, int v) __attribute__((always_inline)) -> vec {
+        if constexpr (XLDS)
+            return xs[(k * V + v) * THREADS + tid];
+        else
+            return xv[k * V + v];
+    };
 
     vec acc[COL ? V : 1];
 #pragma unroll
@@ -280,9 +315,11 @@ k_stream(StreamArgs<T> a)
     vec ra[B][V], rb[B][V];
     vec sa[TWO ? B : 1][V], sb[TWO ? B : 1][V];
     T wa[WTS ? B : 1], wb[WTS ? B : 1];
+    T ua[RANK2 ? 2 * B : 1], ub[RANK2 ? 2 * B : 1];
 
     auto load_batch = [&](int blk, vec (&buf)[B][V], vec (&bbuf)[TWO ? B : 1][V],
-                          T (&wbuf)[WTS ? B : 1]) __attribute__((always_inline)) {
+                          T (&wbuf)[WTS ? B : 1], T (&ubuf)[RANK2 ? 2 * B : 1])
+                          __attribute__((always_inline)) {
 #pragma unroll
         for (int j = 0; j < B; ++j) {
             // first row covered by this wave in batch j, and how many of its rows exist
@@ -308,23 +345,61 @@ k_stream(StreamArgs<T> a)
                     wbuf[j] = load_buf<T, 1, 0>(wr, (uint32_t)sub * ES, 0)[0];
                 }
             }
+            if constexpr (RANK2) {
+                if constexpr (WIDE) {
+                    ubuf[2 * j] = nrows > 0 ? a.u1[r0] : (T)0;
+                    ubuf[2 * j + 1] = nrows > 0 ? a.u2[r0] : (T)0;
+                } else {
+                    const __amdgpu_buffer_rsrc_t r1 = make_rsrc(a.u1 + r0, (uint32_t)(nrows * ES));
+                    const __amdgpu_buffer_rsrc_t r2 = make_rsrc(a.u2 + r0, (uint32_t)(nrows * ES));
+                    ubuf[2 * j] = load_buf<T, 1, 0>(r1, (uint32_t)sub * ES, 0)[0];
+                    ubuf[2 * j + 1] = load_buf<T, 1, 0>(r2, (uint32_t)sub * ES, 0)[0];
+                }
+            }
         }
     };
 
     auto process = [&](int blk, int parity, vec (&buf)[B][V], vec (&bbuf)[TWO ? B : 1][V],
-                       T (&wbuf)[WTS ? B : 1]) __attribute__((always_inline)) {
+                       T (&wbuf)[WTS ? B : 1], T (&ubuf)[RANK2 ? 2 * B : 1])
+                       __attribute__((always_inline)) {
         T d[B], d2[TWO ? B : 1];
+        if constexpr (RANK2) {
+            // Ahat_i = A_i + u1_i v1 + u2_i v2, in the registers that hold A_i;
+            // each slice of v1 and v2 is read once for the whole batch
+#pragma unroll
+            for (int v = 0; v < V; ++v) {
+                const vec v1v = colvec(0, v);
+                const vec v2v = colvec(1, v);
+#pragma unroll
+                for (int j = 0; j < B; ++j)
+#pragma unroll
+                    for (int e = 0; e < VW; ++e)
+                        buf[j][v][e] = fma_t(ubuf[2 * j + 1], v2v[e],
+                                             fma_t(ubuf[2 * j], v1v[e], buf[j][v][e]));
+                if constexpr (XLDS)
+                    __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+        if constexpr (STORE) {
+#pragma unroll
+            for (int j = 0; j < B; ++j) {
+                const int r0 = blk * BR + j * RG + wgrp0;
+                const int left = row_end - r0;
+                const int nrows = left < 0 ? 0 : (left < RPW ? left : RPW);
+                const uint32_t bytes = WIDE ? (nrows > 0 ? pbytes : 0u) : (uint32_t)(nrows * rowbytes);
+                T* orow = a.Aout + (int64_t)r0 * n + col0;
+#pragma unroll
+                for (int v = 0; v < V; ++v)
+                    store_buf<T, VW, AUX>(buf[j][v], rsrc_v(orow, bytes, v), lane_off(v));
+            }
+        }
         if constexpr (DOT) {
 #pragma unroll
             for (int j = 0; j < B; ++j) {
                 T s = 0, s2 = 0;
 #pragma unroll
                 for (int v = 0; v < V; ++v) {
-                    vec xx;
-                    if constexpr (XLDS)
-                        xx = xs[v * THREADS + tid];
-                    else
-                        xx = xv[v];
+                    const vec xx = colvec(0, v);
 #pragma unroll
                     for (int e = 0; e < VW; ++e) {
                         s = fma_t(buf[j][v][e], xx[e], s);
@@ -390,7 +465,7 @@ k_stream(StreamArgs<T> a)
                         } else if constexpr (TWO) {
                             a.rowout[row] = fma_t(a.alpha, d[j], a.beta * d2[j]);
                         } else if (a.rowout != nullptr) {
-                            a.rowout[row] = d[j];
+                            a.rowout[row] = a.scale_rows ? a.alpha * d[j] : d[j];
                         }
                     }
                 }
@@ -436,35 +511,39 @@ k_stream(StreamArgs<T> a)
         bend = nblk;
     }
     row_end = bend * BR < m32 ? bend * BR : m32;
-    // the first batch goes out before the dot vector: x comes from L2 (every
-    // workgroup reads the same slice), the matrix from HBM
+    // the first batch goes out before the column vectors: those come from L2
+    // (every workgroup reads the same slice), the matrix from HBM
     if (blk < bend)
-        load_batch(blk, ra, sa, wa);
-    if constexpr (DOT) {
-        const __amdgpu_buffer_rsrc_t xr = make_rsrc(a.x + col0, pbytes);
+        load_batch(blk, ra, sa, wa, ua);
+    if constexpr (NXV > 0) {
 #pragma unroll
-        for (int v = 0; v < V; ++v) {
-            const int64_t c = (int64_t)(v * G + g) * VW;
-            vec t = load_buf<T, VW, 0>(xr, c < PW ? (uint32_t)(c * ES) : kOutOfRange, 0);
-            if constexpr (XLDS)
-                xs[v * THREADS + tid] = t;
-            else
-                xv[v] = t;
+        for (int k = 0; k < NXV; ++k) {
+            const T* src = DOT ? a.x : (k == 0 ? a.v1 : a.v2);
+            const __amdgpu_buffer_rsrc_t xr = make_rsrc(src + col0, pbytes);
+#pragma unroll
+            for (int v = 0; v < V; ++v) {
+                const int64_t c = (int64_t)(v * G + g) * VW;
+                vec t = load_buf<T, VW, 0>(xr, c < PW ? (uint32_t)(c * ES) : kOutOfRange, 0);
+                if constexpr (XLDS)
+                    xs[(k * V + v) * THREADS + tid] = t;
+                else
+                    xv[k * V + v] = t;
+            }
         }
     }
 
     if (blk < bend) {
         for (;;) {
-            load_batch(blk + bstep, rb, sb, wb);
+            load_batch(blk + bstep, rb, sb, wb, ub);
             __builtin_amdgcn_sched_barrier(0);
-            process(blk, 0, ra, sa, wa);
+            process(blk, 0, ra, sa, wa, ua);
             __builtin_amdgcn_sched_barrier(0);
             blk += bstep;
             if (blk >= bend)
                 break;
-            load_batch(blk + bstep, ra, sa, wa);
+            load_batch(blk + bstep, ra, sa, wa, ua);
             __builtin_amdgcn_sched_barrier(0);
-            process(blk, 1, rb, sb, wb);
+            process(blk, 1, rb, sb, wb, ub);
             __builtin_amdgcn_sched_barrier(0);
             blk += bstep;
             if (blk >= bend)
@@ -514,17 +593,25 @@ k_stream(StreamArgs<T> a)
     }
 }
 
+// Epilogues of the column reduction.
+enum : int {
+    EPI_SCALE = 0,  // out = alpha * sum(P)            (alpha = 1: the plain sum)
+    EPI_TWO = 1,    // out = alpha * sum(P) + beta * sum(Q)
+    EPI_ADDVEC = 2  // out = alpha * sum(P) + Q[j]     (Q a vector of ncols)
+};
+
 // out[j] = sum_{b < nrows} P[b * ldp + j] for j < ncols, rows summed in a fixed
 // order: SL = THREADS / 16 slices of rows (slice s takes rows s, s + SL, ...,
 // sixteen of them per step with their loads issued together, missing rows
-// read as zero), then the slices by a fixed pairwise tree in LDS.  With TWO:
-// out = alpha * sum(P) + beta * sum(Q).  Narrow outputs use 1024 threads, so
-// that many partial rows still take one round of loads.
-template <typename T, int VW, bool TWO, int THREADS = 256>
+// read as zero), then the slices by a fixed pairwise tree in LDS; then the
+// epilogue EPI.  Narrow outputs use 1024 threads, so that many partial rows
+// still take one round of loads.
+template <typename T, int VW, int EPI, int THREADS = 256>
 __global__ void __launch_bounds__(THREADS)
 k_colreduce(const T* __restrict__ P, const T* __restrict__ Q, int64_t ldp, int64_t nrows,
             int64_t ncols, T alpha, T beta, T* __restrict__ out)
 {
+    constexpr bool TWO = EPI == EPI_TWO;
     typedef typename VecOf<T, VW>::type vec;
     constexpr int CV = 16;
     constexpr int SL = THREADS / CV;
@@ -571,11 +658,20 @@ k_colreduce(const T* __restrict__ P, const T* __restrict__ Q, int64_t ldp, int64
     }
     if (sl == 0 && ok) {
         vec t = rp[0][cv];
-        if constexpr (TWO) {
+        if constexpr (EPI == EPI_TWO) {
             const vec t2 = rq[0][cv];
 #pragma unroll
             for (int e = 0; e < VW; ++e)
                 t[e] = fma_t(alpha, t[e], beta * t2[e]);
+        } else if constexpr (EPI == EPI_ADDVEC) {
+            const vec z = load_vec<T, VW>(Q + col);
+#pragma unroll
+            for (int e = 0; e < VW; ++e)
+                t[e] = fma_t(alpha, t[e], z[e]);
+        } else {
+#pragma unroll
+            for (int e = 0; e < VW; ++e)
+                t[e] = alpha * t[e];
         }
         store_vec<T, VW>(out + col, t);
     }

@@ -98,7 +98,8 @@ def ternary(seed: int, array_id: int, shape, dtype=np.float32) -> np.ndarray:
 @dataclass(frozen=True)
 class Workload:
     name: str
-    op: str               # "ata_x" | "bicg" | "axpby_mv" | "matvec" | "matvec_t" | "reduce_sum" | "vector_add"
+    op: str               # "ata_x" | "bicg" | "axpby_mv" | "matvec" | "matvec_t" | "gemver"
+    #                       | "reduce_sum" | "vector_add"
     m: int
     n: int
     seed: int
@@ -145,6 +146,12 @@ WORKLOADS = {
         "vector_add_256m", "vector_add", 1, 1 << 28, 6, "uniform",
         (("a", (1 << 28,)), ("b", (1 << 28,))),
         note="c = a + b, fp32 (2 x 1 GiB in, 1 GiB out): the 'vectoradd' sample of Table 3"),
+    "gemver_16384": Workload(
+        "gemver_16384", "gemver", 16384, 16384, 7, "uniform",
+        (("A", (16384, 16384)), ("u1", (16384,)), ("v1", (16384,)), ("u2", (16384,)),
+         ("v2", (16384,)), ("y", (16384,)), ("z", (16384,))),
+        alpha=1.5, beta=1.2,
+        note="rank-2 update stored, then two products over it, fp32 (1 GiB read, written, read)"),
     "matvec_t_1m_x_64": Workload(
         "matvec_t_1m_x_64", "matvec_t", 1048576, 64, 4, "uniform",
         (("A", (1048576, 64)), ("w", (1048576,))),

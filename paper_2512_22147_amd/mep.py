@@ -21,7 +21,7 @@ LIB_PATH = os.path.join(_HERE, "libmep.so")
 MEP_F32, MEP_F64 = 0, 1
 MEP_OK, MEP_EINVAL, MEP_EALIGN, MEP_EWORKSPACE, MEP_EHIP, MEP_EBUDGET = range(6)
 (MEP_OP_MATVEC, MEP_OP_MATVEC_T, MEP_OP_BICG, MEP_OP_ATA_X, MEP_OP_AXPBY_MV, MEP_OP_REDUCE_SUM,
- MEP_OP_VECTOR_ADD) = range(7)
+ MEP_OP_VECTOR_ADD, MEP_OP_GEMVER) = range(8)
 ERROR_NAMES = {1: "MEP_EINVAL", 2: "MEP_EALIGN", 3: "MEP_EWORKSPACE", 4: "MEP_EHIP", 5: "MEP_EBUDGET"}
 
 # Names exported by libmep.so, in the order include/mep.h declares them.
@@ -30,7 +30,7 @@ EXPORTS = (
     "mep_run", "mep_time_trimmed", "mep_trimmed_mean", "mep_check_fe",
     "mep_variant_count", "mep_set_variant", "mep_variant_info", "mep_profile_begin", "mep_profile_end",
     "mep_stream_copy", "mep_last_error", "mep_version", "mep_select_variant",
-    "mep_reduce_sum", "mep_vector_add",
+    "mep_reduce_sum", "mep_vector_add", "mep_gemver", "mep_profile_end_samples",
 )
 
 
@@ -52,6 +52,8 @@ class MepCall(ctypes.Structure):
         ("ws", ctypes.c_void_p), ("ws_bytes", ctypes.c_size_t),
         ("stream", ctypes.c_void_p),
         ("flush_buf", ctypes.c_void_p), ("flush_bytes", ctypes.c_size_t),
+        ("in2", ctypes.c_void_p), ("in3", ctypes.c_void_p), ("in4", ctypes.c_void_p),
+        ("in5", ctypes.c_void_p), ("out2", ctypes.c_void_p),
     ]
 
 
@@ -94,6 +96,9 @@ def lib() -> ctypes.CDLL:
     L.mep_stream_copy.argtypes = [vp, vp, sz, vp]
     L.mep_reduce_sum.argtypes = [i, i64, vp, vp, vp, sz, vp]
     L.mep_vector_add.argtypes = [i, i64, vp, vp, vp, vp]
+    L.mep_gemver.argtypes = [i, i64, i64, d, d, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    L.mep_profile_end_samples.argtypes = [ctypes.POINTER(d), i, ctypes.POINTER(d),
+                                          ctypes.POINTER(ctypes.c_int)]
     L.mep_select_variant.argtypes = [ctypes.POINTER(MepCall), i, i, i, i, i, d, i,
                                      ctypes.POINTER(ctypes.c_int), ctypes.POINTER(MepCandidateResult), i]
     L.mep_last_error.restype = ctypes.c_char_p
@@ -214,6 +219,23 @@ def mep_axpby_mv(alpha, A, beta, B, x, y=None, ws=None, stream=None):
     return y
 
 
+def mep_gemver(alpha, beta, A, u1, v1, u2, v2, y, z, x=None, w=None, Ahat=None, ws=None, stream=None):
+    """GEMVER: Ahat = A + u1 v1^T + u2 v2^T, x = beta Ahat^T y + z, w = alpha Ahat x.
+
+    Returns (Ahat, x, w).  Pass ``Ahat=A`` for the in-place update."""
+    torch = _torch()
+    m, n = A.shape
+    if Ahat is None:
+        Ahat = torch.empty_like(A)
+    x = _out(A, n, x)
+    w = _out(A, m, w)
+    ws, wsb = _ws(MEP_OP_GEMVER, A, ws)
+    _check(lib().mep_gemver(dtype_code(A.dtype), m, n, float(alpha), float(beta), _ptr(A), _ptr(Ahat),
+                            _ptr(u1), _ptr(v1), _ptr(u2), _ptr(v2), _ptr(y), _ptr(z), _ptr(x), _ptr(w),
+                            _ptr(ws), wsb, _stream(stream)))
+    return Ahat, x, w
+
+
 def mep_reduce_sum(x, s=None, ws=None, stream=None):
     """s = sum of x (one-element tensor)."""
     torch = _torch()
@@ -240,8 +262,11 @@ def mep_vector_add(a, b, c=None, stream=None):
 
 
 def make_call(op, A, in0=None, in1=None, out0=None, out1=None, B=None, alpha=0.0, beta=0.0,
-              ws=None, stream=None, flush_buf=None) -> MepCall:
-    """A mep_call_t over torch tensors (kept alive by the caller)."""
+              ws=None, stream=None, flush_buf=None, in2=None, in3=None, in4=None, in5=None,
+              out2=None) -> MepCall:
+    """A mep_call_t over torch tensors (kept alive by the caller).
+
+    GEMVER: in0..in5 = u1, v1, u2, v2, y, z; out0 = x, out1 = w, out2 = Ahat."""
     if op in (MEP_OP_REDUCE_SUM, MEP_OP_VECTOR_ADD):
         # vector samples: A is the first input vector; m = 1, n = its length
         torch = _torch()
@@ -261,6 +286,7 @@ def make_call(op, A, in0=None, in1=None, out0=None, out1=None, B=None, alpha=0.0
     c.op, c.dtype, c.m, c.n = op, dt, m, n
     c.A, c.B = _ptr(A), _ptr(B)
     c.in0, c.in1, c.out0, c.out1 = _ptr(in0), _ptr(in1), _ptr(out0), _ptr(out1)
+    c.in2, c.in3, c.in4, c.in5, c.out2 = _ptr(in2), _ptr(in3), _ptr(in4), _ptr(in5), _ptr(out2)
     c.alpha, c.beta = float(alpha), float(beta)
     c.ws, c.ws_bytes = _ptr(ws), wsb
     c.stream = _stream(stream)
@@ -349,6 +375,15 @@ def mep_profile_end():
     cnt = ctypes.c_int()
     _check(lib().mep_profile_end(ctypes.byref(tot), ctypes.byref(cnt)))
     return tot.value, cnt.value
+
+
+def mep_profile_end_samples(cap: int = 4096):
+    """Returns (list of per-launch ms in launch order, summed ms, launches)."""
+    tot = ctypes.c_double()
+    cnt = ctypes.c_int()
+    buf = (ctypes.c_double * max(cap, 1))()
+    _check(lib().mep_profile_end_samples(buf, cap, ctypes.byref(tot), ctypes.byref(cnt)))
+    return list(buf[:min(cap, cnt.value)]), tot.value, cnt.value
 
 
 def mep_stream_copy(src, dst, stream=None) -> None:

@@ -7,14 +7,15 @@ import numpy as np
 import oracle
 
 TOL = {np.float32: 1e-4, np.float64: 1e-12}
-OPS = ("matvec", "matvec_t", "bicg", "ata_x", "axpby_mv")
+OPS = ("matvec", "matvec_t", "bicg", "ata_x", "axpby_mv", "gemver")
 
 
 def op_code(op):
     from paper_2512_22147_amd import mep
 
     return {"matvec": mep.MEP_OP_MATVEC, "matvec_t": mep.MEP_OP_MATVEC_T, "bicg": mep.MEP_OP_BICG,
-            "ata_x": mep.MEP_OP_ATA_X, "axpby_mv": mep.MEP_OP_AXPBY_MV}[op]
+            "ata_x": mep.MEP_OP_ATA_X, "axpby_mv": mep.MEP_OP_AXPBY_MV,
+            "gemver": mep.MEP_OP_GEMVER}[op]
 
 
 def make_inputs(op, m, n, dt, seed, kind="uniform"):
@@ -28,6 +29,10 @@ def make_inputs(op, m, n, dt, seed, kind="uniform"):
         ins["w"] = draw(seed, 2, (m,), dt)
     if op == "axpby_mv":
         ins["B"] = draw(seed, 3, (m, n), dt)
+    if op == "gemver":
+        for aid, (name, ln) in enumerate((("u1", m), ("v1", n), ("u2", m), ("v2", n), ("y", m),
+                                          ("z", n)), start=4):
+            ins[name] = draw(seed, aid, (ln,), dt)
     return ins
 
 
@@ -50,6 +55,12 @@ def oracle_outputs(op, ins, dt, alpha=ALPHA, beta=BETA):
         a = oracle.elem_scalar(alpha, dt)
         b = oracle.elem_scalar(beta, dt)
         return {"y": oracle.axpby_mv(a, A, b, ins["B"], ins["x"])}
+    if op == "gemver":
+        a = oracle.elem_scalar(alpha, dt)
+        b = oracle.elem_scalar(beta, dt)
+        Ahat, x, w = oracle.gemver(a, b, A, ins["u1"], ins["v1"], ins["u2"], ins["v2"], ins["y"],
+                                   ins["z"])
+        return {"Ahat": Ahat, "x": x, "w": w}
     raise ValueError(op)
 
 
@@ -75,6 +86,10 @@ def gpu_outputs(op, ins, dt, alpha=ALPHA, beta=BETA, dev=None):
         out = {"y": y, "t": t}
     elif op == "axpby_mv":
         out = {"y": mep.mep_axpby_mv(alpha, T["A"], beta, T["B"], T["x"])}
+    elif op == "gemver":
+        Ahat, x, w = mep.mep_gemver(alpha, beta, T["A"], T["u1"], T["v1"], T["u2"], T["v2"], T["y"],
+                                    T["z"])
+        out = {"Ahat": Ahat, "x": x, "w": w}
     else:
         raise ValueError(op)
     torch.cuda.synchronize()

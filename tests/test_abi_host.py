@@ -32,7 +32,7 @@ def L():
 
 def test_library_exports_every_declared_function(L):
     names = declared_functions()
-    assert len(names) == 20
+    assert len(names) == 22
     for name in names:
         assert hasattr(L, name), f"{name} not exported"
     assert sorted(mep.EXPORTS) == names
@@ -89,6 +89,14 @@ def test_workspace_sizes():
     assert mep.mep_workspace_bytes(mep.MEP_OP_REDUCE_SUM, f32, 1, 0) == 0
     assert mep.mep_workspace_bytes(mep.MEP_OP_VECTOR_ADD, f64, 1, 1000) == 0
     assert mep.mep_variant_count(mep.MEP_OP_REDUCE_SUM, f32, 1, 1000) == 1
+    # GEMVER: pass 1 column partials or pass 2 dot partials, whichever is larger
+    assert ws(mep.MEP_OP_GEMVER, f32, 16384, 16384) >= 64 * 16384 * 4
+    assert ws(mep.MEP_OP_GEMVER, f64, 0, 100) == 0
+    assert ws(mep.MEP_OP_GEMVER, f64, 100, 0) == 0
+    for dt in (f32, f64):
+        for m, n in [(1, 1), (7, 1), (1, 7), (3, 5), (129, 16384), (67, 40000), (4096, 4096)]:
+            assert mep.mep_variant_count(mep.MEP_OP_GEMVER, dt, m, n) >= 1
+            assert ws(mep.MEP_OP_GEMVER, dt, m, n) >= ws(mep.MEP_OP_MATVEC, dt, m, n)
     info = mep.mep_variant_info(mep.MEP_OP_ATA_X, f32, 16384, 16384, 0)
     assert "G=512" in info and "nt" in info
     with pytest.raises(mep.MepError):
@@ -150,6 +158,23 @@ def test_argument_errors(L):
     assert rc == mep.MEP_EINVAL and "overlap" in msg
     rc, msg = _rc(L.mep_vector_add, mep.MEP_F64, 10, FAKE, FAKE * 2, FAKE * 3 + 4, None)
     assert rc == mep.MEP_EALIGN
+    # GEMVER: Ahat may be A itself but must not overlap it otherwise
+    gw = mep.mep_workspace_bytes(mep.MEP_OP_GEMVER, f32, 64, 64)
+    vecs = [FAKE * k for k in range(4, 12)]  # u1, v1, u2, v2, y, z, x, w
+    rc, msg = _rc(L.mep_gemver, f32, 64, 64, 1.0, 1.0, FAKE, FAKE + 64, *vecs, FAKE * 16, gw, None)
+    assert rc == mep.MEP_EINVAL and "overlap" in msg
+    rc, msg = _rc(L.mep_gemver, f32, 64, 64, 1.0, 1.0, FAKE, FAKE * 2, *vecs[:6], None, vecs[7],
+                  FAKE * 16, gw, None)
+    assert rc == mep.MEP_EINVAL and "x" in msg
+    rc, msg = _rc(L.mep_gemver, f32, 64, 64, 1.0, 1.0, FAKE, FAKE * 2, *vecs, FAKE * 16, gw - 1, None)
+    assert rc == mep.MEP_EWORKSPACE
+    rc, msg = _rc(L.mep_gemver, mep.MEP_F64, 64, 64, 1.0, 1.0, FAKE, FAKE * 2, FAKE * 4 + 4, *vecs[1:],
+                  FAKE * 16, gw, None)
+    assert rc == mep.MEP_EALIGN
+    # an output on an input vector
+    rc, msg = _rc(L.mep_gemver, f32, 64, 64, 1.0, 1.0, FAKE, FAKE * 2, *vecs[:6], vecs[5], vecs[7],
+                  FAKE * 16, gw, None)
+    assert rc == mep.MEP_EINVAL and "overlap" in msg
 
 
 def test_harness_errors(L):
@@ -174,5 +199,9 @@ def test_harness_errors(L):
     c.op = mep.MEP_OP_ATA_X
     assert L.mep_select_variant(ctypes.byref(c), 0, 4, 2, 1, 0, 1e-4, 0, ctypes.byref(best), None, 0) == mep.MEP_EBUDGET
     assert L.mep_select_variant(None, 0, 30, 3, 1, 0, 1e-4, 0, ctypes.byref(best), None, 0) == mep.MEP_EINVAL
+    c.op, c.A, c.out2 = mep.MEP_OP_GEMVER, FAKE, FAKE
+    assert L.mep_select_variant(ctypes.byref(c), 0, 30, 3, 1, 0, 1e-4, 0, ctypes.byref(best), None, 0) == mep.MEP_EINVAL
+    assert "out-of-place" in mep.mep_last_error()
+    c.A = c.out2 = None
     c.op = 77
     assert L.mep_select_variant(ctypes.byref(c), 0, 30, 3, 1, 0, 1e-4, 0, ctypes.byref(best), None, 0) == mep.MEP_EINVAL

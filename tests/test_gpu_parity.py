@@ -23,10 +23,10 @@ def _gpu():
         pytest.skip("no GPU")
     from paper_2512_22147_amd import mep
 
-    for op in range(5):
+    for op in range(8):
         mep.mep_set_variant(op, -1)
     yield
-    for op in range(5):
+    for op in range(8):
         mep.mep_set_variant(op, -1)
 
 
@@ -64,6 +64,14 @@ def test_integer_inputs_bit_exact(op, shape, dt):
     m, n = shape
     ins = make_inputs(op, m, n, dt, seed=77 + m, kind="ternary")
     ref = oracle_outputs(op, ins, dt, alpha=1.5, beta=0.25)
+    if op == "gemver":
+        # Ahat is an integer matrix, x a multiple of 1/4, w of 1/8: exact while
+        # every |partial sum| (bounded by |Ahat| |y| and |Ahat| |x|) and every
+        # result stays below 2^24 in those units
+        Ah = np.abs(ref["Ahat"])
+        assert 4 * float(np.max(Ah.T @ np.abs(ins["y"].astype(np.float64)), initial=0)) < 2 ** 24
+        assert 4 * float(np.max(Ah @ np.abs(ref["x"]), initial=0)) < 2 ** 24
+        assert 8 * float(np.max(np.abs(ref["w"]), initial=0)) < 2 ** 24
     got = gpu_outputs(op, ins, dt, alpha=1.5, beta=0.25)
     for k, r in ref.items():
         assert np.array_equal(got[k].astype(np.float64), r), f"{op} {k} not exact"
@@ -109,6 +117,10 @@ def test_misaligned_matrix_takes_elementwise_path(op, dt):
     elif op == "ata_x":
         t = torch.empty(m, dtype=A.dtype, device=dev)
         got = {"y": mep.mep_ata_x(A, x, t=t), "t": t}
+    elif op == "gemver":
+        T = {k: torch.from_numpy(ins[k]).to(dev) for k in ("u1", "v1", "u2", "v2", "y", "z")}
+        Ahat, xo, w = mep.mep_gemver(1.5, 1.2, A, T["u1"], T["v1"], T["u2"], T["v2"], T["y"], T["z"])
+        got = {"Ahat": Ahat, "x": xo, "w": w}
     else:
         rawb = torch.empty_like(raw)
         Bm = rawb[1:].view(m, n)
@@ -141,6 +153,14 @@ def test_empty_sizes(dt):
     assert t.abs().sum() == 0
     assert mep.mep_axpby_mv(1.0, Am0, 1.0, e(6, 0), e(0),
                             y=torch.full((6,), 7.0, dtype=tdt, device=dev)).abs().sum() == 0
+    # GEMVER: no rows gives x = z; no columns gives w = 0
+    z = torch.arange(5, dtype=tdt, device=dev) + 0.5
+    _, xo, w = mep.mep_gemver(1.5, 1.2, A0n, e(0), e(5), e(0), e(5), e(0), z,
+                              x=torch.full((5,), 7.0, dtype=tdt, device=dev))
+    assert torch.equal(xo, z) and w.numel() == 0
+    _, xo, w = mep.mep_gemver(1.5, 1.2, Am0, e(6), e(0), e(6), e(0), e(6), e(0),
+                              w=torch.full((6,), 7.0, dtype=tdt, device=dev))
+    assert xo.numel() == 0 and w.abs().sum() == 0
     torch.cuda.synchronize()
 
 
@@ -163,12 +183,13 @@ def test_guards_and_reproducibility(op):
     guard = 0x5A
     ws_all = torch.full((need + G,), guard, dtype=torch.uint8, device=dev)
     ws = ws_all[:need] if need else None
-    out_len = {"matvec": m, "matvec_t": n, "bicg": n, "ata_x": n, "axpby_mv": m}[op]
+    out_len = {"matvec": m, "matvec_t": n, "bicg": n, "ata_x": n, "axpby_mv": m, "gemver": n}[op]
     sentinel = 12345.0
     runs = []
     for _ in range(2):
         o = torch.full((out_len + G,), sentinel, dtype=torch.float32, device=dev)
         q = torch.full((m + G,), sentinel, dtype=torch.float32, device=dev)
+        hat = torch.full((m * n + G,), sentinel, dtype=torch.float32, device=dev)
         y = o[:out_len]
         if op == "matvec":
             mep.mep_matvec(T["A"], T["x"], y=y, ws=ws)
@@ -178,13 +199,17 @@ def test_guards_and_reproducibility(op):
             mep.mep_matvec_t(T["A"], T["w"], z=y, p=T["x"], q=q[:m], ws=ws)
         elif op == "ata_x":
             mep.mep_ata_x(T["A"], T["x"], y=y, t=q[:m], ws=ws)
+        elif op == "gemver":
+            mep.mep_gemver(1.5, 1.2, T["A"], T["u1"], T["v1"], T["u2"], T["v2"], T["y"], T["z"],
+                           x=y, w=q[:m], Ahat=hat[:m * n].view(m, n), ws=ws)
         else:
             mep.mep_axpby_mv(1.5, T["A"], 1.2, T["B"], T["x"], y=y, ws=ws)
         torch.cuda.synchronize()
         assert bool((o[out_len:] == sentinel).all()), "write past the output"
         assert bool((q[m:] == sentinel).all()), "write past the second output"
+        assert bool((hat[m * n:] == sentinel).all()), "write past the updated matrix"
         assert bool((ws_all[need:] == guard).all()), "write past the workspace"
-        runs.append(torch.cat([y, q[:m]]).cpu().numpy())
+        runs.append(torch.cat([y, q[:m], hat[:m * n] if op == "gemver" else q[:0]]).cpu().numpy())
     assert np.array_equal(runs[0].view(np.uint32), runs[1].view(np.uint32))
 
 
@@ -209,6 +234,21 @@ def test_harness_on_gpu():
         mep.mep_run(call)
     tot, cnt = mep.mep_profile_end()
     assert cnt == 5 and tot > 0
+    # a GEMVER call records both of its streaming passes
+    u = torch.randn(m, device=dev)
+    v = torch.randn(n, device=dev)
+    g = mep.make_call(mep.MEP_OP_GEMVER, A, in0=u, in1=v, in2=u, in3=v, in4=u, in5=v,
+                      out0=torch.empty(n, device=dev), out1=torch.empty(m, device=dev),
+                      out2=torch.empty_like(A), alpha=1.5, beta=1.2)
+    mep.mep_profile_begin(8)
+    for _ in range(3):
+        mep.mep_run(g)
+    samples, tot, cnt = mep.mep_profile_end_samples(8)
+    assert cnt == 6 and len(samples) == 6 and all(t > 0 for t in samples)
+    assert tot == pytest.approx(sum(samples), rel=1e-9)
+    mep.mep_profile_begin(4)
+    with pytest.raises(mep.MepError):
+        mep.mep_profile_end_samples(-1)
     src = torch.arange(1 << 20, dtype=torch.int32, device=dev)
     dst = torch.zeros_like(src)
     mep.mep_stream_copy(src, dst)
@@ -217,7 +257,8 @@ def test_harness_on_gpu():
 
 
 FULL = [("ata_x_1024", "f32"), ("bicg_4096", "f32"), ("axpby_mv_8192", "f32"),
-        ("ata_x_16384", "f32"), ("ata_x_16384", "f64"), ("matvec_t_1m_x_64", "f32")]
+        ("ata_x_16384", "f32"), ("ata_x_16384", "f64"), ("matvec_t_1m_x_64", "f32"),
+        ("gemver_16384", "f32")]
 
 
 @pytest.mark.parametrize("name,dts", FULL, ids=[f"{a}-{b}" for a, b in FULL])
@@ -230,7 +271,7 @@ def test_full_size_workloads(name, dts):
     w = datagen.WORKLOADS[name]
     dt = np.float32 if dts == "f32" else np.float64
     raw = datagen.make_inputs(w, dt)
-    op = {"ata_x": "ata_x", "bicg": "bicg", "axpby_mv": "axpby_mv", "matvec_t": "matvec_t"}[w.op]
+    op = w.op
     if op == "bicg":
         ins = {"A": raw["A"], "x": raw["p"], "w": raw["r"]}
     else:
@@ -244,8 +285,33 @@ def test_full_size_workloads(name, dts):
             assert np.array_equal(got[k], again[k]), f"{k} differs between runs"
 
 
+@pytest.mark.parametrize("dt", DTYPES, ids=["f32", "f64"])
+@pytest.mark.parametrize("shape", [(3000, 4100), (67, 40000), (1000, 1024)],
+                         ids=lambda s: f"{s[0]}x{s[1]}")
+def test_gemver_in_place(shape, dt):
+    """Ahat = A (the in-place update) gives bitwise the out-of-place results."""
+    import torch
+
+    from paper_2512_22147_amd import mep
+
+    m, n = shape
+    ins = make_inputs("gemver", m, n, dt, seed=606 + m)
+    dev = torch.device("cuda:0")
+    T = {k: torch.from_numpy(v).to(dev) for k, v in ins.items()}
+    vecs = [T[k] for k in ("u1", "v1", "u2", "v2", "y", "z")]
+    Ahat, x, w = mep.mep_gemver(1.5, 1.2, T["A"], *vecs)
+    A2 = T["A"].clone()
+    Ahat2, x2, w2 = mep.mep_gemver(1.5, 1.2, A2, *vecs, Ahat=A2)
+    torch.cuda.synchronize()
+    assert Ahat2.data_ptr() == A2.data_ptr()
+    assert torch.equal(Ahat, A2) and torch.equal(x, x2) and torch.equal(w, w2)
+    assert_parity("gemver", {"Ahat": A2.cpu().numpy(), "x": x2.cpu().numpy(), "w": w2.cpu().numpy()},
+                  oracle_outputs("gemver", ins, dt, alpha=1.5, beta=1.2), dt)
+
+
 @pytest.mark.parametrize("op,shape", [("ata_x", (3000, 4096)), ("matvec_t", (100000, 64)),
-                                      ("axpby_mv", (2000, 2048)), ("bicg", (1024, 1024))])
+                                      ("axpby_mv", (2000, 2048)), ("bicg", (1024, 1024)),
+                                      ("gemver", (1000, 2048))])
 def test_select_variant_eqs_3_to_5(op, shape):
     """The Sec. 3.2 selection over the candidate kernels: every candidate
     passes FE against the baseline, the winner is the argmin of the Eq. 3
@@ -263,9 +329,13 @@ def test_select_variant_eqs_3_to_5(op, shape):
     T = {k: torch.from_numpy(v).to(dev) for k, v in ins.items()}
     code = op_code(op)
     out0 = torch.empty(m if op in ("matvec", "axpby_mv") else n, device=dev)
-    out1 = torch.empty(m, device=dev) if op in ("bicg", "ata_x") else None
+    out1 = torch.empty(m, device=dev) if op in ("bicg", "ata_x", "gemver") else None
     kw = dict(out0=out0, out1=out1)
-    if op == "ata_x":
+    if op == "gemver":
+        call = mep.make_call(code, T["A"], in0=T["u1"], in1=T["v1"], in2=T["u2"], in3=T["v2"],
+                             in4=T["y"], in5=T["z"], out2=torch.empty_like(T["A"]), alpha=1.5,
+                             beta=1.2, **kw)
+    elif op == "ata_x":
         call = mep.make_call(code, T["A"], in0=T["x"], **kw)
     elif op == "bicg":
         call = mep.make_call(code, T["A"], in0=T["w"], in1=T["x"], **kw)
