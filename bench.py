@@ -37,11 +37,17 @@ HEADLINE = "ata_x_16384"
 HEADLINE_METRIC = "achieved HBM GB/s (and % of MI355X peak) for y=Aᵀ(Ax), fp32 16384²"
 PEAK_GBS = 8000.0
 KERNEL_SOURCE = "paper_2512_22147_amd/csrc/mep_kernels.hpp"
+VECTOR_KERNEL_SOURCE = "paper_2512_22147_amd/csrc/mep_vector_kernels.hpp"
 
 
-def kernel_source_hash() -> str:
-    with open(os.path.join(ROOT, KERNEL_SOURCE), "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+def kernel_source_hash(workload: str = "") -> str:
+    """Stamp of the source the workload's dominant kernel is built from."""
+    vector = workload.startswith(("reduce_sum", "vector_add"))
+    h = hashlib.sha256()
+    for rel in ((KERNEL_SOURCE, VECTOR_KERNEL_SOURCE) if vector else (KERNEL_SOURCE,)):
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def measured_traffic(workload: str, dtype: str, config: str):
@@ -53,7 +59,7 @@ def measured_traffic(workload: str, dtype: str, config: str):
         return None
     text = open(path).read()
     m = re.search(r"kernel_source_sha256_16:\s*([0-9a-f]+)", text)
-    if not m or m.group(1) != kernel_source_hash():
+    if not m or m.group(1) != kernel_source_hash(workload):
         return None
     m = re.search(rf"config_{dtype}:\s*(.+)", text)
     if not m or m.group(1).strip() != config:
@@ -73,6 +79,8 @@ def parse():
     ap.add_argument("--no-f64", action="store_true", help="skip the fp64 secondary measurement")
     ap.add_argument("--probe-copy", action="store_true",
                     help="also run the 1 GiB streaming-copy probe (counter calibration)")
+    ap.add_argument("--no-ceiling", action="store_true",
+                    help="skip the HBM ceiling probe (a 2 GiB read-sum)")
     ap.add_argument("--variant", type=int, default=-1, help="kernel candidate (Eqs. 4-5); -1 default")
     return ap.parse_args()
 
@@ -268,6 +276,48 @@ def probe_copy():
     return {"bytes_read": nbytes, "bytes_written": nbytes, "gbs": 2 * nbytes / dt / 1e9}
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def probe_ceiling():
+    """HBM read ceiling: the library's sum over ~2 GiB of fp32 (a pure stream;
+    the longest vector the library accepts, 65535 x 8192 elements)."""
+    import torch
+
+    from paper_2512_22147_amd import mep
+
+    dev = torch.device("cuda:0")
+    n = 65535 * 8192
+    x = torch.ones(n, dtype=torch.float32, device=dev)
+    s = torch.empty(1, dtype=torch.float32, device=dev)
+    ws = torch.empty(max(mep.mep_workspace_bytes(mep.MEP_OP_REDUCE_SUM, mep.MEP_F32, 1, n), 1),
+                     dtype=torch.uint8, device=dev)
+    call = mep.make_call(mep.MEP_OP_REDUCE_SUM, x, out0=s, ws=ws)
+    for _ in range(3):
+        mep.mep_run(call)
+    torch.cuda.synchronize()
+    reps = 20
+    mep.mep_profile_begin(reps)
+    for _ in range(reps):
+        mep.mep_run(call)
+    torch.cuda.synchronize()
+    tot, cnt = mep.mep_profile_end()
+    gbs = n * 4 / (tot / cnt * 1e-3) / 1e9
+    log(f"[bench] HBM ceiling probe: sum of {n * 4} B fp32, {gbs:.1f} GB/s")
+    del x, ws
+    torch.cuda.empty_cache()
+    return {"kernel": "k_reduce_sum (fp32, 65535 x 8192 elements)", "bytes_read": n * 4, "gbs": round(gbs, 1),
+            "frac_of_peak": round(gbs / PEAK_GBS, 4)}
+
+
 def cpu_baseline(res):
     import numpy as np
 
@@ -275,10 +325,15 @@ def cpu_baseline(res):
 
     w, host = res["w"], res["host"]
     host64 = {k: np.ascontiguousarray(v, dtype=np.float64) for k, v in host.items()}
-    R, k = 3, 1
+    threads = oracle.default().num_threads()
+    # Eq. 3 with R = 30, k = 3 when one call is short, else R = 5, k = 1:
+    # a bounded sample of a few seconds to ~30 s of host time
+    t0 = time.perf_counter()
+    ref = oracle_outputs(w, host64, res["dtype"])
+    first = time.perf_counter() - t0
+    R, k = (30, 3) if first * 30 <= 30.0 else (5, 1)
+    log(f"[bench] CPU oracle ({cpu_model()}): {R} calls on {threads} threads")
     times = []
-    ref = None
-    log(f"[bench] CPU oracle: {R} calls on {oracle.default().num_threads()} threads")
     for _ in range(R):
         t0 = time.perf_counter()
         ref = oracle_outputs(w, host64, res["dtype"])
@@ -286,10 +341,10 @@ def cpu_baseline(res):
     t = oracle.trimmed_mean(times, k)
     shape = "x".join(str(s) for s in next(iter(host.values())).shape)
     return {
-        "value": res["alg_bytes_step"] / t / 1e9, "unit": "GB/s", "cores": oracle.default().num_threads(),
-        "kind": "oracle", "seconds_per_call": t,
+        "value": res["alg_bytes_step"] / t / 1e9, "unit": "GB/s", "cores": threads,
+        "kind": "oracle", "seconds_per_call": t, "cpu_model": cpu_model(),
         "sample": f"the full {w.name} workload ({shape} {res['dtype']}; inputs promoted to fp64 "
-                  f"before timing), {R} calls, Eq. 3 trimmed mean with k={k}",
+                  f"before timing), {R} calls after one untimed, Eq. 3 trimmed mean with k={k}",
     }, ref
 
 
@@ -347,6 +402,7 @@ def main():
             "kernel_config": sec["config"],
         }
     copy = probe_copy() if args.probe_copy else None
+    ceiling = None if args.no_ceiling else probe_ceiling()
     w = prim["w"]
     desc = OPS[w.op][2]
     metric = (HEADLINE_METRIC if args.workload == HEADLINE and args.dtype == "f32"
@@ -382,6 +438,8 @@ def main():
         "fe_error_vs_oracle": fe,
         "secondary": secondary,
         "copy_probe": copy,
+        "hbm_ceiling_probe": ceiling,
+        "kernel_frac_of_ceiling": None if ceiling is None else round(prim["kernel_gbs"] / ceiling["gbs"], 4),
     }
     print(json.dumps(out), flush=True)
 

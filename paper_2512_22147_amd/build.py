@@ -30,7 +30,7 @@ HIP_FLAGS = [
 ]
 SOURCES = ["mep_api.hip", "mep_launch_f32.hip", "mep_launch_f64.hip", "mep_launch_f32_wide.hip",
            "mep_launch_f64_wide.hip"]
-HEADERS = ["mep_kernels.hpp", "mep_internal.hpp", "mep_launch.inc"]
+HEADERS = ["mep_kernels.hpp", "mep_vector_kernels.hpp", "mep_internal.hpp", "mep_launch.inc"]
 
 
 def _run(cmd, verbose):

@@ -677,90 +677,6 @@ k_colreduce(const T* __restrict__ P, const T* __restrict__ Q, int64_t ldp, int64
     }
 }
 
-// Sum of a vector, first stage: workgroup b adds the 16-byte vectors of its
-// own contiguous chunk (lanes stride by 256 vectors, four loads in flight per
-// lane, non-temporal), then its lanes (butterfly) and its four waves
-// (ascending) into partial[b].  The trailing n mod VW elements are added by
-// the first lanes of workgroup 0.  The order depends only on n and
-// gridDim.x, so the result is reproducible; k_colreduce with one column adds
-// the partials.
-template <typename T, int VW>
-__global__ void __launch_bounds__(256)
-k_reduce_sum(const T* __restrict__ x, int64_t n, T* __restrict__ partial)
-{
-    typedef typename VecOf<T, VW>::type vec;
-    constexpr int U = 4;
-    const vec* xv = reinterpret_cast<const vec*>(x);
-    const int64_t nv = n / VW;
-    const int64_t chunk = (nv + gridDim.x - 1) / gridDim.x;
-    const int64_t b0 = (int64_t)blockIdx.x * chunk;
-    const int64_t b1 = b0 + chunk < nv ? b0 + chunk : nv;
-    int64_t i = b0 + threadIdx.x;
-    vec acc = (vec)(T)0;
-    for (; i + (U - 1) * 256 < b1; i += U * 256) {
-        vec t[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u)
-            t[u] = __builtin_nontemporal_load(xv + i + u * 256);
-#pragma unroll
-        for (int u = 0; u < U; ++u)
-            acc += t[u];
-    }
-    for (; i < b1; i += 256)
-        acc += __builtin_nontemporal_load(xv + i);
-    T s = 0;
-#pragma unroll
-    for (int e = 0; e < VW; ++e)
-        s += acc[e];
-    if (blockIdx.x == 0 && (int64_t)threadIdx.x < n - nv * VW)
-        s += x[nv * VW + threadIdx.x];
-    s = group_sum<64>(s);
-    __shared__ T red[4];
-    if ((threadIdx.x & 63) == 0)
-        red[threadIdx.x >> 6] = s;
-    lds_barrier();
-    if (threadIdx.x == 0)
-        partial[blockIdx.x] = ((red[0] + red[1]) + red[2]) + red[3];
-}
-
-// c = a + b elementwise: workgroup b handles its own contiguous chunk of
-// 16-byte vectors (lanes stride by 256 vectors, four in flight per lane),
-// with non-temporal loads and stores; the trailing n mod VW elements by
-// workgroup 0.
-template <typename T, int VW>
-__global__ void __launch_bounds__(256)
-k_vector_add(const T* __restrict__ a, const T* __restrict__ b, T* __restrict__ c, int64_t n)
-{
-    typedef typename VecOf<T, VW>::type vec;
-    constexpr int U = 4;
-    const vec* av = reinterpret_cast<const vec*>(a);
-    const vec* bv = reinterpret_cast<const vec*>(b);
-    vec* cv = reinterpret_cast<vec*>(c);
-    const int64_t nv = n / VW;
-    const int64_t chunk = (nv + gridDim.x - 1) / gridDim.x;
-    const int64_t b0 = (int64_t)blockIdx.x * chunk;
-    const int64_t b1 = b0 + chunk < nv ? b0 + chunk : nv;
-    int64_t i = b0 + threadIdx.x;
-    for (; i + (U - 1) * 256 < b1; i += U * 256) {
-        vec ta[U], tb[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            ta[u] = __builtin_nontemporal_load(av + i + u * 256);
-            tb[u] = __builtin_nontemporal_load(bv + i + u * 256);
-        }
-#pragma unroll
-        for (int u = 0; u < U; ++u)
-            __builtin_nontemporal_store(ta[u] + tb[u], cv + i + u * 256);
-    }
-    for (; i < b1; i += 256)
-        __builtin_nontemporal_store(__builtin_nontemporal_load(av + i) + __builtin_nontemporal_load(bv + i),
-                                    cv + i);
-    if (blockIdx.x == 0 && (int64_t)threadIdx.x < n - nv * VW) {
-        const int64_t k = nv * VW + threadIdx.x;
-        c[k] = a[k] + b[k];
-    }
-}
-
 // Zero-fill of count elements (outputs of empty sums).
 template <typename T>
 __global__ void __launch_bounds__(256) k_fill_zero(T* __restrict__ p, int64_t count)
