@@ -383,6 +383,8 @@ def main():
     if args.workload not in datagen.WORKLOADS:
         print(f"unknown workload {args.workload}; known: {sorted(datagen.WORKLOADS)}", file=sys.stderr)
         sys.exit(2)
+    # the ceiling first: HBM throughput read right after minutes of streaming is a few % lower
+    ceiling = None if args.no_ceiling else probe_ceiling()
     prim = run_gpu(args.workload, args.dtype, args.steps, args.warmup, args.variant)
     fe = None
     cpu = None
@@ -402,7 +404,6 @@ def main():
             "kernel_config": sec["config"],
         }
     copy = probe_copy() if args.probe_copy else None
-    ceiling = None if args.no_ceiling else probe_ceiling()
     w = prim["w"]
     desc = OPS[w.op][2]
     metric = (HEADLINE_METRIC if args.workload == HEADLINE and args.dtype == "f32"

@@ -66,17 +66,23 @@ static Cfg preferred_shape(int mode, int esize, int64_t m, int64_t n, int64_t nv
         return Cfg{64, 1, 8, 4, aux};
     if (nv <= 256)
         return Cfg{64, 4, 2, 4, aux};
-    // the rank-2 update that stores Ahat: 1024-lane groups (panels past 4096 vectors)
+    // the rank-2 update that stores Ahat: 1024-lane groups on every compute
+    // unit (panels past 4096 vectors)
     if (mode & F_STORE)
         return Cfg{1024, 4, 2, 4, aux};
-    if (nv <= 4096)
-        return Cfg{512, 8, 2, 2, aux};
+    // one streamed matrix of 4096-vector rows: 22 (ATAX) or 24 compute units
+    // per XCD; two matrices (half the rows per batch) and longer rows keep all 32
+    if (nv <= 4096) {
+        const int cux = !stream || (mode & F_TWO) ? kCusPerXcd : ((mode & F_FROMDOT) ? 22 : 24);
+        return Cfg{512, 8, 2, 2, aux, 0, cux};
+    }
     return Cfg{512, 16, 1, 2, aux};
 }
 
 static bool same_cfg(const Cfg& a, const Cfg& b)
 {
-    return a.G == b.G && a.V == b.V && a.B == b.B && a.WPE == b.WPE && a.AUX == b.AUX && a.MAP == b.MAP;
+    return a.G == b.G && a.V == b.V && a.B == b.B && a.WPE == b.WPE && a.AUX == b.AUX && a.MAP == b.MAP &&
+           a.CUX == b.CUX;
 }
 
 int stream_candidates(int esize, bool vec, int mode, int64_t m, int64_t n, int* idx)
@@ -142,9 +148,9 @@ Plan plan_stream(int esize, bool vec, int mode, int64_t m, int64_t n, int varian
     p.panels = std::max<int64_t>(1, (n + p.pw - 1) / p.pw);
     const int64_t rows_per_block = (int64_t)batch_of(p.c.B, mode) * (p.threads / p.c.G);
     const int64_t nblk = (m + rows_per_block - 1) / rows_per_block;
-    // enough workgroups to fill the 256 compute units at the shape's occupancy
+    // enough workgroups to fill the shape's CUX compute units per XCD at its occupancy
     const int64_t per_cu = p.threads <= 256 ? 4 : (p.threads == 512 && p.c.WPE >= 4 ? 2 : 1);
-    p.nb = std::max<int64_t>(1, std::min<int64_t>(nblk, 256 * per_cu));
+    p.nb = std::max<int64_t>(1, std::min<int64_t>(nblk, (int64_t)kXcds * p.c.CUX * per_cu));
     return p;
 }
 
@@ -651,7 +657,7 @@ int mep_variant_count(int op, int dtype, int64_t m, int64_t n)
 {
     const int es = esize_of(dtype);
     if (is_vector_op(op))
-        return (es == 0 || n < 0 || n > kMaxDim) ? 0 : 1;
+        return (es == 0 || n < 0 || n > kMaxDim) ? 0 : (op == MEP_OP_VECTOR_ADD ? kNumVaddVariants : 1);
     const int mode = op_mode(op);
     if (es == 0 || mode < 0 || m < 0 || n < 0 || m > kMaxDim || n > kMaxDim)
         return 0;
@@ -664,13 +670,18 @@ int mep_variant_info(int op, int dtype, int64_t m, int64_t n, int variant, char*
 {
     const int es = esize_of(dtype);
     if (is_vector_op(op)) {
-        if (es == 0 || n < 0 || n > kMaxDim || variant != 0 || buf == nullptr || buf_len == 0)
+        const int count = mep_variant_count(op, dtype, m, n);
+        if (es == 0 || n < 0 || n > kMaxDim || variant < 0 || variant >= count || buf == nullptr ||
+            buf_len == 0)
             return fail(MEP_EINVAL, "bad arguments to mep_variant_info");
         if (op == MEP_OP_REDUCE_SUM)
             snprintf(buf, buf_len, "reduce threads=256 grid=%lld, fixed-order partials",
                      (long long)reduce_blocks(n, es));
+        else if (variant == 0)
+            snprintf(buf, buf_len, "vector-add chunks threads=256, 16-byte non-temporal");
         else
-            snprintf(buf, buf_len, "vector-add threads=256, 16-byte non-temporal");
+            snprintf(buf, buf_len, "vector-add rows threads=1024 V=4 cus=%d/%d, 16-byte non-temporal",
+                     variant == 1 ? kCusPerXcd : (variant == 2 ? 24 : 16), kCusPerXcd);
         return MEP_OK;
     }
     const int mode = op_mode(op);
@@ -683,10 +694,10 @@ int mep_variant_info(int op, int dtype, int64_t m, int64_t n, int variant, char*
     if (variant < 0 || variant >= cnt)
         return fail(MEP_EINVAL, "variant %d outside 0..%d", variant, cnt - 1);
     const Plan p = plan_stream(es, vec, mode, m, n, variant);
-    snprintf(buf, buf_len, "%s G=%d V=%d B=%d WPE=%d %s %s threads=%d grid=%lldx%lld",
+    snprintf(buf, buf_len, "%s G=%d V=%d B=%d WPE=%d %s %s cus=%d/%d threads=%d grid=%lldx%lld",
              vec ? "vec16" : "elem", p.c.G, p.c.V, batch_of(p.c.B, mode), p.c.WPE,
-             p.c.AUX ? "nt" : "cached", p.c.MAP ? "blocked" : "cyclic", p.threads, (long long)p.nb,
-             (long long)p.panels);
+             p.c.AUX ? "nt" : "cached", p.c.MAP ? "blocked" : "cyclic", p.c.CUX, kCusPerXcd, p.threads,
+             (long long)p.nb, (long long)p.panels);
     return MEP_OK;
 }
 
@@ -893,9 +904,10 @@ int mep_vector_add(int dtype, int64_t n, const void* a, const void* b, void* c, 
         return MEP_OK;
     hipStream_t s = (hipStream_t)stream;
     const LaunchEvents ev = prof_next();
+    const int v = std::max(0, variant_of(MEP_OP_VECTOR_ADD));
     const hipError_t e =
-        dtype == MEP_F32 ? launch_vector_add<float>((const float*)a, (const float*)b, (float*)c, n, s, ev)
-                         : launch_vector_add<double>((const double*)a, (const double*)b, (double*)c, n, s, ev);
+        dtype == MEP_F32 ? launch_vector_add<float>((const float*)a, (const float*)b, (float*)c, n, v, s, ev)
+                         : launch_vector_add<double>((const double*)a, (const double*)b, (double*)c, n, v, s, ev);
     return e == hipSuccess ? MEP_OK : hip_fail(e, "vector add launch");
 }
 

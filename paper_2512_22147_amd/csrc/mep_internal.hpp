@@ -13,29 +13,37 @@ namespace mep {
 // Row-group geometry of one streaming-kernel instance: G lanes per row
 // group, V vectors per lane, B rows per batch, WPE waves per SIMD (the
 // register budget is 512 / WPE per lane), AUX the cache-policy bits of the
-// matrix loads (0 = default, 2 = non-temporal streaming).  MAP (a launch
-// argument, not part of the instance) hands row blocks to workgroups
-// cyclically (0) or in contiguous runs (1).
+// matrix loads (0 = default, 2 = non-temporal streaming).  MAP and CUX are
+// launch arguments, not part of the instance: MAP hands row blocks to
+// workgroups cyclically (0) or in contiguous runs (1); CUX is how many of
+// each XCD's 32 compute units the grid is sized for (workgroups are dealt to
+// the 8 XCDs in turn).  Measured on MI355X, streaming one large fp32 matrix
+// from 22-24 compute units per XCD beats all 32 (fewer rows in flight at
+// once); with two matrices, or fp64 rows, all 32 are as fast or faster.
 struct Cfg {
-    int G, V, B, WPE, AUX, MAP = 0;
+    int G, V, B, WPE, AUX, MAP = 0, CUX = 32;
 };
+
+constexpr int kXcds = 8;
+constexpr int kCusPerXcd = 32;
 
 // Vector path (16-byte loads), ordered by row capacity G * V; among equal
 // capacities the preferred shape comes first (measured on MI355X: streaming
 // the matrix with non-temporal loads is faster for every shape).
-constexpr int kNumVecCfg = 30;
+constexpr int kNumVecCfg = 35;
 constexpr Cfg kVecCfg[kNumVecCfg] = {
     {16, 1, 8, 4, 2},    {16, 1, 8, 4, 0},    {64, 1, 8, 4, 2},    {64, 1, 8, 4, 0},
     {64, 2, 4, 4, 2},    {64, 2, 4, 4, 0},    {64, 4, 2, 4, 2},    {64, 4, 2, 4, 0},
     {256, 2, 4, 4, 2},   {256, 2, 4, 4, 0},   {256, 4, 2, 4, 2},   {256, 4, 2, 4, 0},
     {1024, 2, 4, 4, 2},  {1024, 2, 4, 4, 0},
     // 4096 vectors: a 16384-element fp32 row
-    {512, 8, 2, 2, 2},   {512, 8, 2, 2, 2, 1}, {1024, 4, 2, 4, 2},  {512, 8, 1, 4, 2},
-    {256, 16, 1, 2, 2},  {512, 8, 2, 2, 0},    {1024, 4, 2, 4, 0},  {512, 8, 1, 4, 0},
-    {256, 16, 1, 2, 0},
+    {512, 8, 2, 2, 2, 0, 24}, {512, 8, 2, 2, 2, 0, 22}, {512, 8, 2, 2, 2}, {512, 8, 2, 2, 2, 1},
+    {1024, 4, 2, 4, 2},  {1024, 4, 2, 4, 2, 0, 24}, {512, 8, 1, 4, 2}, {256, 16, 1, 2, 2},
+    {512, 8, 2, 2, 0},   {1024, 4, 2, 4, 0},   {512, 8, 1, 4, 0},   {256, 16, 1, 2, 0},
     // 8192 vectors: a 16384-element fp64 row or a 32768-element fp32 row
-    {512, 16, 1, 2, 2},  {512, 16, 1, 2, 2, 1}, {1024, 8, 1, 4, 2},  {256, 32, 1, 1, 2},
-    {512, 16, 1, 2, 0},  {1024, 8, 1, 4, 0},   {256, 32, 1, 1, 0}};
+    {512, 16, 1, 2, 2, 0, 26}, {512, 16, 1, 2, 2, 0, 24}, {512, 16, 1, 2, 2}, {512, 16, 1, 2, 2, 1},
+    {1024, 8, 1, 4, 2},  {256, 32, 1, 1, 2},   {512, 16, 1, 2, 0},  {1024, 8, 1, 4, 0},
+    {256, 32, 1, 1, 0}};
 // Element-wise path (rows not 16-byte aligned): one element per load.
 constexpr int kNumScalarCfg = 3;
 constexpr Cfg kScalarCfg[kNumScalarCfg] = {{64, 4, 2, 4, 2}, {256, 4, 2, 4, 2}, {1024, 8, 1, 4, 2}};
@@ -131,7 +139,8 @@ template <typename T>
 hipError_t launch_reduce_sum(const T* x, int64_t n, T* out, T* partial, int64_t nb, hipStream_t s,
                              const LaunchEvents& ev);
 template <typename T>
-hipError_t launch_vector_add(const T* a, const T* b, T* c, int64_t n, hipStream_t s, const LaunchEvents& ev);
+hipError_t launch_vector_add(const T* a, const T* b, T* c, int64_t n, int variant, hipStream_t s,
+                             const LaunchEvents& ev);
 template <>
 hipError_t launch_reduce_sum<float>(const float*, int64_t, float*, float*, int64_t, hipStream_t,
                                     const LaunchEvents&);
@@ -139,11 +148,16 @@ template <>
 hipError_t launch_reduce_sum<double>(const double*, int64_t, double*, double*, int64_t, hipStream_t,
                                      const LaunchEvents&);
 template <>
-hipError_t launch_vector_add<float>(const float*, const float*, float*, int64_t, hipStream_t,
+hipError_t launch_vector_add<float>(const float*, const float*, float*, int64_t, int, hipStream_t,
                                     const LaunchEvents&);
 template <>
-hipError_t launch_vector_add<double>(const double*, const double*, double*, int64_t, hipStream_t,
+hipError_t launch_vector_add<double>(const double*, const double*, double*, int64_t, int, hipStream_t,
                                      const LaunchEvents&);
+
+// Candidate launches of the vector add: 0 = contiguous chunk per workgroup,
+// 1-3 = row-streamed with 1024-lane workgroups on 32, 24 or 16 compute units
+// per XCD.
+constexpr int kNumVaddVariants = 4;
 
 hipError_t launch_copy16(const void* src, void* dst, size_t bytes, hipStream_t s);
 hipError_t launch_flush(void* buf, size_t bytes, uint32_t tag, hipStream_t s);

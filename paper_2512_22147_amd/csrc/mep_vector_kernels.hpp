@@ -92,4 +92,60 @@ k_vector_add(const T* __restrict__ a, const T* __restrict__ b, T* __restrict__ c
     }
 }
 
+// c = a + b, row-streamed: the vectors are read as rows of THREADS * V
+// 16-byte vectors (64 KiB of each input for 1024 x 4); workgroup w takes rows
+// w, w + gridDim.x, ..., so the grid sweeps one contiguous window at a time,
+// and the next row of a and b is loaded while the current one is added and
+// stored.  Every access is guarded by the vector count; the trailing n mod VW
+// elements go to the first lanes of workgroup 0.
+template <typename T, int VW, int V, int THREADS>
+__global__ void __launch_bounds__(THREADS)
+k_vector_add_rows(const T* __restrict__ a, const T* __restrict__ b, T* __restrict__ c, int64_t n)
+{
+    typedef typename VecOf<T, VW>::type vec;
+    const vec* av = reinterpret_cast<const vec*>(a);
+    const vec* bv = reinterpret_cast<const vec*>(b);
+    vec* cv = reinterpret_cast<vec*>(c);
+    const int64_t nv = n / VW;
+    constexpr int64_t RV = (int64_t)THREADS * V;
+    const int64_t rows = (nv + RV - 1) / RV;
+    const int tid = threadIdx.x;
+    const vec zero = (vec)(T)0;
+    vec xa[V], xb[V], ya[V], yb[V];
+    auto load = [&](int64_t r, vec (&pa)[V], vec (&pb)[V]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int v = 0; v < V; ++v) {
+            const int64_t i = r * RV + (int64_t)v * THREADS + tid;
+            pa[v] = i < nv ? __builtin_nontemporal_load(av + i) : zero;
+            pb[v] = i < nv ? __builtin_nontemporal_load(bv + i) : zero;
+        }
+    };
+    auto store = [&](int64_t r, vec (&pa)[V], vec (&pb)[V]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int v = 0; v < V; ++v) {
+            const int64_t i = r * RV + (int64_t)v * THREADS + tid;
+            if (i < nv)
+                __builtin_nontemporal_store(pa[v] + pb[v], cv + i);
+        }
+    };
+    const int64_t step = gridDim.x;
+    int64_t r = blockIdx.x;
+    if (r < rows)
+        load(r, xa, xb);
+    while (r < rows) {
+        load(r + step, ya, yb);
+        store(r, xa, xb);
+        r += step;
+        if (r >= rows)
+            break;
+        load(r + step, xa, xb);
+        store(r, ya, yb);
+        r += step;
+    }
+    if (blockIdx.x == 0 && (int64_t)tid < n - nv * VW) {
+        const int64_t k = nv * VW + tid;
+        c[k] = a[k] + b[k];
+    }
+}
+
 }  // namespace mep

@@ -22,6 +22,11 @@ def _gpu():
 
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
+    from paper_2512_22147_amd import mep
+
+    mep.mep_set_variant(mep.MEP_OP_VECTOR_ADD, -1)
+    yield
+    mep.mep_set_variant(mep.MEP_OP_VECTOR_ADD, -1)
 
 
 def _dev(a, offset=0):
@@ -81,12 +86,17 @@ def test_vector_add_bit_exact(n, dt, offset):
     b = datagen.normal(920 + n % 89, 1, (n,), dt)
     ref = oracle.vector_add(a, b).astype(dt)
     guard = 4096
-    c_all = torch.full((n + guard,), 777.0, dtype=torch.float32 if dt == np.float32 else torch.float64,
-                       device="cuda:0")
-    c = mep.mep_vector_add(_dev(a, offset), _dev(b, offset), c=c_all[:n])
-    torch.cuda.synchronize()
-    assert np.array_equal(c.cpu().numpy(), ref)
-    assert bool((c_all[n:] == 777.0).all()), "write past c"
+    ad, bd = _dev(a, offset), _dev(b, offset)
+    count = mep.mep_variant_count(mep.MEP_OP_VECTOR_ADD, mep.MEP_F32 if dt == np.float32 else mep.MEP_F64, 1, n)
+    assert count >= 2
+    for v in range(count):
+        mep.mep_set_variant(mep.MEP_OP_VECTOR_ADD, v)
+        c_all = torch.full((n + guard,), 777.0, dtype=torch.float32 if dt == np.float32 else torch.float64,
+                           device="cuda:0")
+        c = mep.mep_vector_add(ad, bd, c=c_all[:n])
+        torch.cuda.synchronize()
+        assert np.array_equal(c.cpu().numpy(), ref), f"candidate {v}"
+        assert bool((c_all[n:] == 777.0).all()), f"candidate {v} wrote past c"
 
 
 @pytest.mark.parametrize("name", ["reduce_sum_256m", "vector_add_256m"])
@@ -106,7 +116,10 @@ def test_vector_workloads_full_size(name):
         scale = float(np.abs(x.astype(np.float64)).sum())
         assert abs(float(got.cpu()[0]) - ref) <= 1e-4 * scale
     else:
-        c = mep.mep_vector_add(_dev(ins["a"]), _dev(ins["b"]))
-        torch.cuda.synchronize()
         ref = oracle.vector_add(ins["a"], ins["b"]).astype(np.float32)
-        assert np.array_equal(c.cpu().numpy(), ref)
+        ad, bd = _dev(ins["a"]), _dev(ins["b"])
+        for v in range(mep.mep_variant_count(mep.MEP_OP_VECTOR_ADD, mep.MEP_F32, 1, ad.numel())):
+            mep.mep_set_variant(mep.MEP_OP_VECTOR_ADD, v)
+            c = mep.mep_vector_add(ad, bd)
+            torch.cuda.synchronize()
+            assert np.array_equal(c.cpu().numpy(), ref), f"candidate {v}"
