@@ -30,9 +30,10 @@ constexpr int kCusPerXcd = 32;
 // Vector path (16-byte loads), ordered by row capacity G * V; among equal
 // capacities the preferred shape comes first (measured on MI355X: streaming
 // the matrix with non-temporal loads is faster for every shape).
-constexpr int kNumVecCfg = 35;
+constexpr int kNumVecCfg = 37;
 constexpr Cfg kVecCfg[kNumVecCfg] = {
-    {16, 1, 8, 4, 2},    {16, 1, 8, 4, 0},    {64, 1, 8, 4, 2},    {64, 1, 8, 4, 0},
+    {16, 1, 8, 4, 2},    {16, 1, 8, 4, 2, 0, 24}, {16, 1, 8, 4, 2, 0, 16}, {16, 1, 8, 4, 0},
+    {64, 1, 8, 4, 2},    {64, 1, 8, 4, 0},
     {64, 2, 4, 4, 2},    {64, 2, 4, 4, 0},    {64, 4, 2, 4, 2},    {64, 4, 2, 4, 0},
     {256, 2, 4, 4, 2},   {256, 2, 4, 4, 0},   {256, 4, 2, 4, 2},   {256, 4, 2, 4, 0},
     {1024, 2, 4, 4, 2},  {1024, 2, 4, 4, 0},
