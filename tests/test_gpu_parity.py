@@ -167,7 +167,7 @@ def test_empty_sizes(dt):
 @pytest.mark.parametrize("op", OPS)
 def test_guards_and_reproducibility(op):
     """Nothing is written past the outputs or the workspace, and two runs give
-    bitwise-identical results (fixed-order reductions, no atomics)."""
+    bitwise-identical results (fixed-order reductions)."""
     import torch
 
     from paper_2512_22147_amd import mep
@@ -349,3 +349,27 @@ def test_select_variant_eqs_3_to_5(op, shape):
     assert best == oracle.select_next([(i, t, ok) for i, (t, _, ok) in enumerate(res)])
     got = gpu_outputs(op, ins, dt)
     assert_parity(op, got, oracle_outputs(op, ins, dt), dt, what=f"selected candidate {best}")
+
+
+@pytest.mark.parametrize("dt", DTYPES, ids=["f32", "f64"])
+@pytest.mark.parametrize("op", ["matvec_t", "bicg", "ata_x", "gemver"])
+@pytest.mark.parametrize("shape", [(200000, 64), (150001, 7), (300000, 128), (70000, 1)],
+                         ids=lambda s: f"{s[0]}x{s[1]}")
+def test_narrow_outputs_split_reduce(op, shape, dt):
+    """Many rows, few columns: hundreds of partial rows of a narrow output
+    and the element-wise path for odd widths.  Every candidate against the
+    oracle, and three runs bit for bit alike."""
+    from paper_2512_22147_amd import mep
+
+    m, n = shape
+    ins = make_inputs(op, m, n, dt, seed=4242 + n)
+    ref = oracle_outputs(op, ins, dt)
+    code = op_code(op)
+    count = mep.mep_variant_count(code, mep.MEP_F32 if dt == np.float32 else mep.MEP_F64, m, n)
+    for v in range(count):
+        mep.mep_set_variant(code, v)
+        runs = [gpu_outputs(op, ins, dt) for _ in range(3)]
+        assert_parity(op, runs[0], ref, dt, what=f"{m}x{n} candidate {v}")
+        for k in ref:
+            assert runs[0][k].tobytes() == runs[1][k].tobytes() == runs[2][k].tobytes(), \
+                f"{op} {k} candidate {v} differs between runs"
