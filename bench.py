@@ -326,25 +326,29 @@ def cpu_baseline(res):
     w, host = res["w"], res["host"]
     host64 = {k: np.ascontiguousarray(v, dtype=np.float64) for k, v in host.items()}
     threads = oracle.default().num_threads()
-    # Eq. 3 with R = 30, k = 3 when one call is short, else R = 5, k = 1:
-    # a bounded sample of a few seconds to ~30 s of host time
+    # Eq. 3 (R = 30, k = 3); each sample is `inner` back-to-back calls, sized
+    # so that the whole sample is ~10 s of host time (R = 5, k = 1 when one
+    # call alone is longer than 1 s)
     t0 = time.perf_counter()
     ref = oracle_outputs(w, host64, res["dtype"])
     first = time.perf_counter() - t0
-    R, k = (30, 3) if first * 30 <= 30.0 else (5, 1)
-    log(f"[bench] CPU oracle ({cpu_model()}): {R} calls on {threads} threads")
+    R, k = (30, 3) if first <= 1.0 else (5, 1)
+    inner = max(1, int(round(10.0 / (R * max(first, 1e-6)))))
+    log(f"[bench] CPU oracle ({cpu_model()}): {R} samples of {inner} calls on {threads} threads")
     times = []
     for _ in range(R):
         t0 = time.perf_counter()
-        ref = oracle_outputs(w, host64, res["dtype"])
-        times.append(time.perf_counter() - t0)
+        for _ in range(inner):
+            ref = oracle_outputs(w, host64, res["dtype"])
+        times.append((time.perf_counter() - t0) / inner)
     t = oracle.trimmed_mean(times, k)
     shape = "x".join(str(s) for s in next(iter(host.values())).shape)
     return {
         "value": res["alg_bytes_step"] / t / 1e9, "unit": "GB/s", "cores": threads,
         "kind": "oracle", "seconds_per_call": t, "cpu_model": cpu_model(),
         "sample": f"the full {w.name} workload ({shape} {res['dtype']}; inputs promoted to fp64 "
-                  f"before timing), {R} calls after one untimed, Eq. 3 trimmed mean with k={k}",
+                  f"before timing): {R} samples of {inner} back-to-back calls ({R * inner} calls, "
+                  f"~{R * inner * t:.0f} s) after one untimed call, Eq. 3 trimmed mean with k={k}",
     }, ref
 
 
