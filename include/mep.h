@@ -204,7 +204,7 @@ int mep_time_trimmed(const mep_call_t* call, int warmup, int R, int k, int inner
 double mep_trimmed_mean(const double* samples, int R, int k);
 
 /*
- * Functional-equivalence check (Eq. 4, "output consistency"): compares the
+ * Functional-equivalence check (Eq. 4; the paper asks that outputs agree): compares the
  * host copy `out` (len elements of dtype) with a host fp64 reference.
  * *err = max_i |out_i - ref_i| / max_i |ref_i| (normwise relative error);
  * +inf if any out_i is not finite, or if ref is all zero and out is not.

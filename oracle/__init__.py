@@ -20,7 +20,7 @@ Contents
   k lowest and k highest, average the remaining R - 2k; only defined for
   R > 2k.
 * ``fe_error`` / ``fe_pass``: the functional-equivalence test of Eq. 4 under
-  this build's reading of "output consistency": the normwise relative error
+  this build's reading of the paper's requirement that outputs agree: the normwise relative error
   max_i |out_i - ref_i| / max_i |ref_i|; any non-finite output fails; an
   all-zero reference demands an all-zero output.
 * ``select_next`` : Eqs. 4-5 -- among the candidates that pass FE, the one with
