@@ -73,13 +73,13 @@ static Cfg preferred_shape(int mode, int esize, int64_t m, int64_t n, int64_t nv
     // unit (panels past 4096 vectors)
     if (mode & F_STORE)
         return Cfg{1024, 4, 2, 4, aux};
-    // one streamed matrix of 4096-vector rows: 22 (ATAX) or 24 compute units
-    // per XCD; two matrices (half the rows per batch) and longer rows keep all 32
-    if (nv <= 4096) {
-        const int cux = !stream || (mode & F_TWO) ? kCusPerXcd : ((mode & F_FROMDOT) ? 22 : 24);
-        return Cfg{512, 8, 2, 2, aux, 0, cux};
-    }
-    return Cfg{512, 16, 1, 2, aux};
+    // one streamed matrix: 22 (ATAX) or 24 compute units per XCD for 4096-vector
+    // rows, 26 for 8192-vector rows; two matrices (half the rows per batch)
+    // keep all 32
+    const bool narrow_grid = stream && !(mode & F_TWO);
+    if (nv <= 4096)
+        return Cfg{512, 8, 2, 2, aux, 0, narrow_grid ? ((mode & F_FROMDOT) ? 22 : 24) : kCusPerXcd};
+    return Cfg{512, 16, 1, 2, aux, 0, narrow_grid ? 26 : kCusPerXcd};
 }
 
 static bool same_cfg(const Cfg& a, const Cfg& b)

@@ -17,9 +17,9 @@ namespace mep {
 // launch arguments, not part of the instance: MAP hands row blocks to
 // workgroups cyclically (0) or in contiguous runs (1); CUX is how many of
 // each XCD's 32 compute units the grid is sized for (workgroups are dealt to
-// the 8 XCDs in turn).  Measured on MI355X, streaming one large fp32 matrix
-// from 22-24 compute units per XCD beats all 32 (fewer rows in flight at
-// once); with two matrices, or fp64 rows, all 32 are as fast or faster.
+// the 8 XCDs in turn).  Measured on MI355X, streaming one large matrix from
+// 22-26 compute units per XCD beats all 32 (fewer rows in flight at once);
+// with two matrices all 32 are faster.
 struct Cfg {
     int G, V, B, WPE, AUX, MAP = 0, CUX = 32;
 };
