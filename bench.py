@@ -14,6 +14,9 @@ device synchronizations.  One JSON line is printed:
                   its average duration, from event pairs stamped by each launch
                   of the timed region on the kernel's own stream; traffic is
                   the calibrated rocprofv3 HBM byte count per launch
+* eq3          -- the MEP timing rule of Eq. 3 on the GPU: 3 warm-up calls,
+                  R = 30 samples, each after a 1 GiB cache flush, trimmed
+                  mean with the k = 3 fastest and slowest dropped
 * cpu_baseline -- the CPU oracle, as it stands, on the host cores
 
 Other workloads (--workload): ata_x_1024, bicg_4096, axpby_mv_8192,
@@ -82,6 +85,8 @@ def parse():
     ap.add_argument("--no-ceiling", action="store_true",
                     help="skip the HBM ceiling probe (a 2 GiB read-sum)")
     ap.add_argument("--variant", type=int, default=-1, help="kernel candidate (Eqs. 4-5); -1 default")
+    ap.add_argument("--no-eq3", action="store_true",
+                    help="skip the Eq. 3 cold-cache timing (R = 30, k = 3, 1 GiB flush per sample)")
     return ap.parse_args()
 
 
@@ -202,7 +207,35 @@ def oracle_outputs(w, host, dtype):
     return {"c": oracle.vector_add(host["a"], host["b"])}
 
 
-def run_gpu(workload: str, dtype: str, steps: int, warmup: int, variant: int):
+# Eq. 3 as the MEP harness applies it (Sec. 3.2, R = 30 and k = 3 from Sec. 4.1.3;
+# three untimed warm-up calls): each sample is one call (or `inner` back-to-back
+# calls when one call is shorter than T_min) timed by events on the call's stream,
+# after a 1 GiB write that evicts every operand from the caches.
+EQ3 = {"warmup": 3, "R": 30, "k": 3, "flush_bytes": 1 << 30}
+
+
+def eq3_timing(S, ms_step):
+    import math
+
+    import torch
+
+    from paper_2512_22147_amd import mep
+
+    flush = torch.empty(EQ3["flush_bytes"], dtype=torch.uint8, device=torch.device("cuda:0"))
+    call = S["call"]
+    call.flush_buf, call.flush_bytes = flush.data_ptr(), EQ3["flush_bytes"]
+    inner = max(1, math.ceil(T_MIN_MS / ms_step))
+    mean_ms, samples = mep.mep_time_trimmed(call, warmup=EQ3["warmup"], R=EQ3["R"], k=EQ3["k"],
+                                            inner=inner, flush=True)
+    call.flush_buf, call.flush_bytes = None, 0
+    del flush
+    gbs = S["alg_step"] / (mean_ms * 1e-3) / 1e9
+    return {**EQ3, "inner": inner, "trimmed_mean_ms": round(mean_ms, 5),
+            "min_ms": round(min(samples), 5), "max_ms": round(max(samples), 5),
+            "gbs": round(gbs, 1), "frac": round(gbs / PEAK_GBS, 4)}
+
+
+def run_gpu(workload: str, dtype: str, steps: int, warmup: int, variant: int, eq3_flush: bool = True):
     import torch
 
     from paper_2512_22147_amd import mep
@@ -225,8 +258,9 @@ def run_gpu(workload: str, dtype: str, steps: int, warmup: int, variant: int):
     kern = S["kernels"]
     samples, kern_ms, launches = mep.mep_profile_end_samples(steps * len(kern) + 16)
     config = mep.mep_variant_info(code, mep.dtype_code(S["tdt"]), S["m"], S["n"], max(variant, 0))
-    mep.mep_set_variant(code, -1)
     ms_step = elapsed * 1e3 / steps
+    eq3 = eq3_timing(S, ms_step) if eq3_flush else None
+    mep.mep_set_variant(code, -1)
     per_kernel = []
     if launches == steps * len(kern):
         # launch position p of every step is the same kernel
@@ -244,7 +278,7 @@ def run_gpu(workload: str, dtype: str, steps: int, warmup: int, variant: int):
         "value_gbs": S["alg_step"] / (ms_step * 1e-3) / 1e9,
         "kernel_ms": dom["ms"], "kernel_launches": launches, "kernel_name": dom["kernel"],
         "kernel_gbs": dom["gbs"], "per_kernel": per_kernel if len(per_kernel) > 1 else None,
-        "alg_bytes_step": S["alg_step"], "alg_bytes_kernel": dom["alg_bytes"], "config": config,
+        "alg_bytes_step": S["alg_step"], "alg_bytes_kernel": dom["alg_bytes"], "config": config, "eq3": eq3,
         "outs": {k: v.cpu().numpy() for k, v in S["outs"]().items()},
         "host": S["host"], "w": S["w"],
     }
@@ -407,7 +441,7 @@ def main():
     # the ceiling first: HBM throughput read right after minutes of streaming is a few % lower
     ceiling = None if args.no_ceiling else probe_ceiling()
     t_mep = time.perf_counter()
-    prim = run_gpu(args.workload, args.dtype, args.steps, args.warmup, args.variant)
+    prim = run_gpu(args.workload, args.dtype, args.steps, args.warmup, args.variant, not args.no_eq3)
     # the MEP proper: input generation, upload, warm-up and timed steps
     t_mep = time.perf_counter() - t_mep
     fe = None
@@ -418,14 +452,14 @@ def main():
     prim.pop("host")
     secondary = None
     if args.workload == HEADLINE and not args.no_f64 and args.dtype == "f32":
-        sec = run_gpu(args.workload, "f64", args.steps, args.warmup, args.variant)
+        sec = run_gpu(args.workload, "f64", args.steps, args.warmup, args.variant, not args.no_eq3)
         secondary = {
             "dtype": "f64", "value": round(sec["value_gbs"], 1), "unit": "GB/s",
             "ms_per_step": round(sec["ms_per_step"], 4),
             "kernel_gbs": round(sec["kernel_gbs"], 1),
             "frac_of_peak": round(sec["kernel_gbs"] / PEAK_GBS, 4),
             "traffic": measured_traffic(args.workload, "f64", sec["config"]),
-            "kernel_config": sec["config"],
+            "kernel_config": sec["config"], "eq3": sec["eq3"],
         }
     copy = probe_copy() if args.probe_copy else None
     w = prim["w"]
@@ -459,6 +493,7 @@ def main():
         "per_kernel": None if prim["per_kernel"] is None else [
             {"kernel": k["kernel"], "ms": round(k["ms"], 5), "alg_bytes": k["alg_bytes"],
              "gbs": round(k["gbs"], 1), "frac": round(k["gbs"] / PEAK_GBS, 4)} for k in prim["per_kernel"]],
+        "eq3": prim["eq3"],
         "cpu_baseline": cpu,
         "fe_error_vs_oracle": fe,
         "secondary": secondary,

@@ -50,14 +50,21 @@ constexpr int64_t kMaxRow = int64_t(65535) * 8192;
 
 static int esize_of(int dtype) { return dtype == MEP_F32 ? 4 : (dtype == MEP_F64 ? 8 : 0); }
 
-// The default shape for a row of nv vectors, from measurements on MI355X
-// (candidate sweeps over the five benchmark workloads): the narrowest row
-// group for very short rows, 512-lane groups with 8 or 16 vectors per lane
-// otherwise.  Matrices that stay resident in the 256 MB Infinity Cache across
-// calls are read with cached loads; larger ones are streamed non-temporally.
+// The default shape for a row of nv vectors, from candidate sweeps on MI355X
+// over row lengths of 512-8192 vectors, both element types, every operation,
+// and matrices that stay in the 256 MB Infinity Cache (32-64 MiB) or stream
+// from HBM (1 GiB).  What decides the shape is how much of each row group
+// holds data and how many bytes every compute unit keeps in flight: 512-lane
+// groups with batches of 4-8 rows win wherever a row is up to 2048 vectors,
+// and the 16384-element fp32 rows of the benchmark want 512 lanes x 8
+// vectors on 22-24 compute units per XCD.  Large matrices are streamed with
+// non-temporal loads; cache-resident ones mostly read faster cached, except
+// where a sweep showed otherwise (noted below).
 static Cfg preferred_shape(int mode, int esize, int64_t m, int64_t n, int64_t nv)
 {
-    const int64_t mats = (mode & F_TWO) ? 2 : 1;
+    const bool two = (mode & F_TWO) != 0;
+    const bool col = (mode & F_COL) != 0;
+    const int64_t mats = two ? 2 : 1;
     const bool stream = mats * m * n * esize > (int64_t(128) << 20);
     const int aux = stream ? 2 : 0;
     // rows of <= 16 vectors: 16 compute units per XCD (512 workgroups) halve
@@ -73,13 +80,39 @@ static Cfg preferred_shape(int mode, int esize, int64_t m, int64_t n, int64_t nv
     // unit (panels past 4096 vectors)
     if (mode & F_STORE)
         return Cfg{1024, 4, 2, 4, aux};
-    // one streamed matrix: 22 (ATAX) or 24 compute units per XCD for 4096-vector
-    // rows, 26 for 8192-vector rows; two matrices (half the rows per batch)
-    // keep all 32
-    const bool narrow_grid = stream && !(mode & F_TWO);
-    if (nv <= 4096)
-        return Cfg{512, 8, 2, 2, aux, 0, narrow_grid ? ((mode & F_FROMDOT) ? 22 : 24) : kCusPerXcd};
-    return Cfg{512, 16, 1, 2, aux, 0, narrow_grid ? 26 : kCusPerXcd};
+    const bool bicg64 = mode == MODE_BICG && esize == 8;  // the most registers per row
+    if (nv <= 512) {
+        if (!stream)  // cached: y = A x and GESUMMV on 256-lane groups
+            return mode == MODE_MV || two ? Cfg{256, 2, 4, 4, 0} : Cfg{512, 2, 8, 2, 0};
+        if (bicg64)
+            return Cfg{512, 1, 8, 4, 2};
+        return mode == MODE_ATW || two ? Cfg{512, 2, 8, 2, 2} : Cfg{512, 2, 4, 4, 2};
+    }
+    if (nv <= 1024) {  // non-temporal even where cached: measured faster
+        if (!stream && (mode == MODE_MV || two))
+            return Cfg{256, 4, 2, 4, 2};
+        return bicg64 && stream ? Cfg{512, 2, 8, 2, 2} : Cfg{512, 4, 4, 2, 2};
+    }
+    if (nv <= 2048) {
+        if (!stream)
+            return Cfg{512, 4, 4, 2, col ? 0 : 2};
+        if (mode == MODE_MV)
+            return Cfg{512, 8, 1, 4, 2};
+        return Cfg{512, 8, 2, 2, 2};  // every compute unit: the narrow grid is ~15% slower here
+    }
+    // Longer rows.  Streamed: one matrix on 22 (ATAX) or 24 compute units per
+    // XCD for 4096-vector rows, 26 for 8192-vector rows; two matrices (half
+    // the rows per batch, 4096-vector column panels) on 22 for 4096-vector
+    // rows and all 32 beyond.  Cached: y = A x and GESUMMV still read
+    // non-temporally (~10% faster), the column-sum modes cached.
+    const int laux = stream || !col ? 2 : 0;
+    if (nv <= 4096 || two) {
+        const int cux = !stream ? kCusPerXcd
+                        : two ? (nv <= 4096 ? 22 : kCusPerXcd)
+                              : ((mode & F_FROMDOT) ? 22 : 24);
+        return Cfg{512, 8, 2, 2, laux, 0, cux};
+    }
+    return Cfg{512, 16, 1, 2, laux, 0, stream ? 26 : kCusPerXcd};
 }
 
 static bool same_cfg(const Cfg& a, const Cfg& b)

@@ -30,13 +30,18 @@ constexpr int kCusPerXcd = 32;
 // Vector path (16-byte loads), ordered by row capacity G * V; among equal
 // capacities the preferred shape comes first (measured on MI355X: streaming
 // the matrix with non-temporal loads is faster for every shape).
-constexpr int kNumVecCfg = 37;
+constexpr int kNumVecCfg = 44;
 constexpr Cfg kVecCfg[kNumVecCfg] = {
     {16, 1, 8, 4, 2},    {16, 1, 8, 4, 2, 0, 24}, {16, 1, 8, 4, 2, 0, 16}, {16, 1, 8, 4, 0},
     {64, 1, 8, 4, 2},    {64, 1, 8, 4, 0},
     {64, 2, 4, 4, 2},    {64, 2, 4, 4, 0},    {64, 4, 2, 4, 2},    {64, 4, 2, 4, 0},
-    {256, 2, 4, 4, 2},   {256, 2, 4, 4, 0},   {256, 4, 2, 4, 2},   {256, 4, 2, 4, 0},
-    {1024, 2, 4, 4, 2},  {1024, 2, 4, 4, 0},
+    // 512 vectors
+    {256, 2, 4, 4, 2},   {256, 2, 4, 4, 0},   {512, 1, 8, 4, 2},
+    // 1024 vectors
+    {256, 4, 2, 4, 2},   {256, 4, 2, 4, 0},   {512, 2, 8, 2, 2},   {512, 2, 8, 2, 0},
+    {512, 2, 4, 4, 2},   {1024, 1, 8, 4, 2},
+    // 2048 vectors
+    {1024, 2, 4, 4, 2},  {1024, 2, 4, 4, 0},  {512, 4, 4, 2, 2},   {512, 4, 4, 2, 0},
     // 4096 vectors: a 16384-element fp32 row
     {512, 8, 2, 2, 2, 0, 24}, {512, 8, 2, 2, 2, 0, 22}, {512, 8, 2, 2, 2}, {512, 8, 2, 2, 2, 1},
     {1024, 4, 2, 4, 2},  {1024, 4, 2, 4, 2, 0, 24}, {512, 8, 1, 4, 2}, {256, 16, 1, 2, 2},

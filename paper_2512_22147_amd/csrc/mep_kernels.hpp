@@ -423,7 +423,8 @@ k_stream(StreamArgs<T> a)
                         d2[j] = group_sum<G>(d2[j]);
                 }
             } else {
-                const int wig = wave % WPG;  // wave index inside the row group
+                static_assert(RG == 1, "a row group wider than a wave spans the whole workgroup");
+                const int wig = wave;  // wave index inside the row group
 #pragma unroll
                 for (int j = 0; j < B; ++j) {
                     d[j] = group_sum<64>(d[j]);
@@ -439,18 +440,50 @@ k_stream(StreamArgs<T> a)
                     }
                 }
                 lds_barrier();
+                // The table holds NROW rows of WPG wave partials.
+                constexpr int NROW = NDOT * B;
+                if constexpr (NROW * WPG <= 16 && WPE <= 2) {
+                    // small table and a large register budget: every lane adds
+                    // each row's partials in wave order
 #pragma unroll
-                for (int j = 0; j < B; ++j) {
-                    T s = 0, s2 = 0;
+                    for (int j = 0; j < B; ++j) {
+                        T s = 0, s2 = 0;
 #pragma unroll
-                    for (int w = 0; w < WPG; ++w) {
-                        s += red[parity][j * WPG + w];
+                        for (int w = 0; w < WPG; ++w) {
+                            s += red[parity][j * WPG + w];
+                            if constexpr (TWO)
+                                s2 += red[parity][(B + j) * WPG + w];
+                        }
+                        d[j] = s;
                         if constexpr (TWO)
-                            s2 += red[parity][(B + j) * WPG + w];
+                            d2[j] = s2;
                     }
-                    d[j] = s;
-                    if constexpr (TWO)
-                        d2[j] = s2;
+                } else {
+                    // larger tables: lane l of every wave takes entry l (and
+                    // l + 64, ...), a butterfly over each aligned group of WPG
+                    // lanes adds one row's partials, and the row totals are
+                    // read back as wave-uniform values.  One LDS read per lane
+                    // instead of NROW * WPG reads and as many live registers,
+                    // which made the 8-row batches of 512 and 1024-lane groups
+                    // spill.
+                    constexpr int NCH = (NROW * WPG + 63) / 64;
+                    T part[NCH];
+#pragma unroll
+                    for (int ch = 0; ch < NCH; ++ch) {
+                        const int i = ch * 64 + lane;
+                        part[ch] = i < NROW * WPG ? red[parity][i] : (T)0;
+                        part[ch] = group_sum<WPG>(part[ch]);
+                    }
+#pragma unroll
+                    for (int k = 0; k < NROW; ++k) {
+                        const T tot = lanes_apply(part[k * WPG / 64], [&](int x) {
+                            return __builtin_amdgcn_readlane(x, (k * WPG) % 64);
+                        });
+                        if (k < B)
+                            d[k] = tot;
+                        else if constexpr (TWO)
+                            d2[k - B] = tot;
+                    }
                 }
             }
             if (g == 0) {
