@@ -76,10 +76,19 @@ static Cfg preferred_shape(int mode, int esize, int64_t m, int64_t n, int64_t nv
         return Cfg{64, 1, 8, 4, aux};
     if (nv <= 256)
         return Cfg{64, 4, 2, 4, aux};
-    // the rank-2 update that stores Ahat: 1024-lane groups on every compute
-    // unit (panels past 4096 vectors)
-    if (mode & F_STORE)
+    // the rank-2 update that stores Ahat (GEMVER's first pass): 512-lane groups
+    // sized to the row up to 2048 vectors (fp64 rows of <= 512 vectors on
+    // 256 x 4, where 512 x 2 x 8 spills), 1024-lane groups with 4 vectors per
+    // lane beyond (panels past 4096 vectors)
+    if (mode & F_STORE) {
+        if (nv <= 512)
+            return stream && esize == 8 ? Cfg{256, 4, 2, 4, 2} : Cfg{512, 2, 8, 2, aux};
+        if (nv <= 1024)
+            return stream ? Cfg{512, 4, 4, 2, 2} : Cfg{512, 2, 8, 2, 0};
+        if (nv <= 2048)
+            return stream ? Cfg{512, 8, 2, 2, 2} : Cfg{512, 4, 4, 2, 0};
         return Cfg{1024, 4, 2, 4, aux};
+    }
     const bool bicg64 = mode == MODE_BICG && esize == 8;  // the most registers per row
     if (nv <= 512) {
         if (!stream)  // cached: y = A x and GESUMMV on 256-lane groups

@@ -107,6 +107,46 @@ def test_workspace_sizes():
         mep.mep_variant_info(mep.MEP_OP_ATA_X, f32, 16384, 16384, 99)
 
 
+# Default shapes measured on MI355X (candidate sweeps over row lengths, element
+# types, operations, streamed 1 GiB and cache-resident 32-64 MiB matrices):
+# (op, dtype, m, n) -> the shape candidate 0 must have.  A change of the rule
+# has to come with a sweep that justifies it.
+MEASURED_DEFAULTS = [
+    # the benchmark workloads
+    ("ATA_X", 0, 16384, 16384, "G=512 V=8 B=2 WPE=2 nt cyclic cus=22/32"),
+    ("ATA_X", 1, 16384, 16384, "G=512 V=16 B=1 WPE=2 nt cyclic cus=26/32"),
+    ("ATA_X", 0, 1024, 1024, "G=64 V=4 B=2 WPE=4 cached"),
+    ("BICG", 0, 4096, 4096, "G=512 V=4 B=4 WPE=2 nt cyclic cus=32/32"),
+    ("AXPBY_MV", 0, 8192, 8192, "G=512 V=8 B=1 WPE=2 nt cyclic cus=32/32"),
+    ("MATVEC_T", 0, 1 << 20, 64, "G=16 V=1 B=8 WPE=4 nt cyclic cus=16/32"),
+    ("GEMVER", 0, 16384, 16384, "G=1024 V=4 B=2 WPE=4 nt cyclic cus=32/32"),
+    ("MATVEC", 0, 16384, 16384, "G=512 V=8 B=2 WPE=2 nt cyclic cus=24/32"),
+    # other row lengths, streamed
+    ("ATA_X", 0, 65536, 4096, "G=512 V=4 B=4 WPE=2 nt cyclic cus=32/32"),
+    ("MATVEC_T", 0, 131072, 2048, "G=512 V=2 B=8 WPE=2 nt"),
+    ("MATVEC", 0, 131072, 2048, "G=512 V=2 B=4 WPE=4 nt"),
+    ("BICG", 1, 131072, 1024, "G=512 V=1 B=8 WPE=4 nt"),
+    ("MATVEC", 0, 32768, 8192, "G=512 V=8 B=1 WPE=4 nt"),
+    ("BICG", 0, 32768, 8192, "G=512 V=8 B=2 WPE=2 nt cyclic cus=32/32"),
+    ("AXPBY_MV", 0, 8192, 16384, "G=512 V=8 B=1 WPE=2 nt cyclic cus=22/32"),
+    ("GEMVER", 0, 131072, 2048, "G=512 V=2 B=8 WPE=2 nt"),
+    ("GEMVER", 1, 131072, 1024, "G=256 V=4 B=2 WPE=4 nt"),
+    # cache-resident
+    ("MATVEC", 0, 4096, 2048, "G=256 V=2 B=4 WPE=4 cached"),
+    ("ATA_X", 0, 4096, 2048, "G=512 V=2 B=8 WPE=2 cached"),
+    ("AXPBY_MV", 0, 2048, 4096, "G=256 V=4 B=1 WPE=4 nt"),
+    ("MATVEC", 0, 1024, 16384, "G=512 V=8 B=2 WPE=2 nt cyclic cus=32/32"),
+    ("BICG", 0, 1024, 16384, "G=512 V=8 B=2 WPE=2 cached"),
+]
+
+
+@pytest.mark.parametrize("op,dt,m,n,want", MEASURED_DEFAULTS,
+                         ids=[f"{c[0]}-{'f32' if c[1] == 0 else 'f64'}-{c[2]}x{c[3]}" for c in MEASURED_DEFAULTS])
+def test_measured_default_shapes(op, dt, m, n, want):
+    info = mep.mep_variant_info(getattr(mep, f"MEP_OP_{op}"), dt, m, n, 0)
+    assert want in info, info
+
+
 def _rc(fn, *args):
     rc = fn(*args)
     return rc, mep.mep_last_error()
