@@ -97,11 +97,22 @@ static Cfg preferred_shape(int mode, int esize, int64_t m, int64_t n, int64_t nv
             return Cfg{512, 1, 8, 4, 2};
         return mode == MODE_ATW || two ? Cfg{512, 2, 8, 2, 2} : Cfg{512, 2, 4, 4, 2};
     }
+    // Past 512 vectors a row group of 512 lanes takes V vectors per lane, V the
+    // power of two that makes 512 x V cover the row at least half full, and
+    // B = 16 / V rows per batch (the same vectors in flight whatever the row
+    // length).  Where the row fills more than 7/8 of that capacity, the sweeps
+    // found the next shape (the row twice over, half the rows per batch) a few
+    // % faster, and keep it there; lower in a range it leaves 3/4 of each
+    // group idle and runs up to 40% slower.
+    if (nv <= 896)
+        return two && !stream ? Cfg{256, 4, 2, 4, 2} : Cfg{512, 2, 8, 2, aux};
     if (nv <= 1024) {  // non-temporal even where cached: measured faster
         if (!stream && (mode == MODE_MV || two))
             return Cfg{256, 4, 2, 4, 2};
         return bicg64 && stream ? Cfg{512, 2, 8, 2, 2} : Cfg{512, 4, 4, 2, 2};
     }
+    if (nv <= 1792)
+        return Cfg{512, 4, 4, 2, stream || !col ? 2 : 0};
     if (nv <= 2048) {
         if (!stream)
             return Cfg{512, 4, 4, 2, col ? 0 : 2};
@@ -109,19 +120,22 @@ static Cfg preferred_shape(int mode, int esize, int64_t m, int64_t n, int64_t nv
             return Cfg{512, 8, 1, 4, 2};
         return Cfg{512, 8, 2, 2, 2};  // every compute unit: the narrow grid is ~15% slower here
     }
-    // Longer rows.  Streamed: one matrix on 22 (ATAX) or 24 compute units per
-    // XCD for 4096-vector rows, 26 for 8192-vector rows; two matrices (half
-    // the rows per batch, 4096-vector column panels) on 22 for 4096-vector
-    // rows and all 32 beyond.  Cached: y = A x and GESUMMV still read
-    // non-temporally (~10% faster), the column-sum modes cached.
+    // Longer rows.  Streamed rows that fill their group more than 7/8: one
+    // matrix on 22 (ATAX) or 24 compute units per XCD for 4096-vector rows, 26
+    // for 8192-vector rows; two matrices (half the rows per batch,
+    // 4096-vector column panels) on 22 for 4096-vector rows and all 32
+    // beyond.  Emptier groups keep fewer bytes in flight and use every
+    // compute unit.  Cached: y = A x and GESUMMV still read non-temporally
+    // (~10% faster), the column-sum modes cached.
     const int laux = stream || !col ? 2 : 0;
+    const bool full = (nv > 3584 && nv <= 4096) || nv > 7168;
     if (nv <= 4096 || two) {
-        const int cux = !stream ? kCusPerXcd
+        const int cux = !stream || !full ? kCusPerXcd
                         : two ? (nv <= 4096 ? 22 : kCusPerXcd)
                               : ((mode & F_FROMDOT) ? 22 : 24);
         return Cfg{512, 8, 2, 2, laux, 0, cux};
     }
-    return Cfg{512, 16, 1, 2, laux, 0, stream ? 26 : kCusPerXcd};
+    return Cfg{512, 16, 1, 2, laux, 0, stream && full ? 26 : kCusPerXcd};
 }
 
 static bool same_cfg(const Cfg& a, const Cfg& b)

@@ -131,6 +131,10 @@ MEASURED_DEFAULTS = [
     ("AXPBY_MV", 0, 8192, 16384, "G=512 V=8 B=1 WPE=2 nt cyclic cus=22/32"),
     ("GEMVER", 0, 131072, 2048, "G=512 V=2 B=8 WPE=2 nt"),
     ("GEMVER", 1, 131072, 1024, "G=256 V=4 B=2 WPE=4 nt"),
+    # rows between the measured lengths: the smallest 512-lane shape that covers them
+    ("ATA_X", 0, 65472, 4100, "G=512 V=4 B=4 WPE=2 nt cyclic cus=32/32"),
+    ("BICG", 0, 87267, 3076, "G=512 V=2 B=8 WPE=2 nt"),
+    ("ATA_X", 0, 21838, 12292, "G=512 V=8 B=2 WPE=2 nt cyclic cus=32/32"),
     # cache-resident
     ("MATVEC", 0, 4096, 2048, "G=256 V=2 B=4 WPE=4 cached"),
     ("ATA_X", 0, 4096, 2048, "G=512 V=2 B=8 WPE=2 cached"),
