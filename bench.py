@@ -85,6 +85,9 @@ def parse():
     ap.add_argument("--no-ceiling", action="store_true",
                     help="skip the HBM ceiling probe (a 2 GiB read-sum)")
     ap.add_argument("--variant", type=int, default=-1, help="kernel candidate (Eqs. 4-5); -1 default")
+    ap.add_argument("--select", action="store_true",
+                    help="also run one round of candidate selection (Eqs. 3-5, cold cache) and report "
+                         "the chosen shape's standalone speedup over the default (Sec. 4.1.3)")
     ap.add_argument("--no-eq3", action="store_true",
                     help="skip the Eq. 3 cold-cache timing (R = 30, k = 3, 1 GiB flush per sample)")
     return ap.parse_args()
@@ -233,6 +236,33 @@ def eq3_timing(S, ms_step):
     return {**EQ3, "inner": inner, "trimmed_mean_ms": round(mean_ms, 5),
             "min_ms": round(min(samples), 5), "max_ms": round(max(samples), 5),
             "gbs": round(gbs, 1), "frac": round(gbs / PEAK_GBS, 4)}
+
+
+def select_round(workload: str, dtype: str):
+    """One round of the paper's loop over the library's candidate shapes: FE
+    against the baseline (candidate 0), Eq. 3 timing with a cache flush per
+    sample, argmin (Eqs. 4-5); the speedup counts only an FE-passing winner."""
+    import torch
+
+    from paper_2512_22147_amd import mep, report
+
+    S = setup(workload, dtype)
+    flush = torch.empty(EQ3["flush_bytes"], dtype=torch.uint8, device=torch.device("cuda:0"))
+    call = S["call"]
+    call.flush_buf, call.flush_bytes = flush.data_ptr(), EQ3["flush_bytes"]
+    tol = 1e-4 if dtype == "f32" else 1e-12
+    best, res = mep.mep_select_variant(call, warmup=EQ3["warmup"], R=EQ3["R"], k=EQ3["k"], flush=True,
+                                       tol=tol, apply=False)
+    dt = mep.dtype_code(S["tdt"])
+    out = {"candidates": len(res), "fe_passed": sum(1 for r in res if r[2]), "best": best,
+           "best_config": mep.mep_variant_info(S["code"], dt, S["m"], S["n"], max(best, 0)),
+           "baseline_config": mep.mep_variant_info(S["code"], dt, S["m"], S["n"], 0),
+           "baseline_ms": round(res[0][0], 5), "best_ms": round(res[best][0], 5) if best >= 0 else None,
+           "standalone_speedup": report.selection_speedup(res, best)}
+    log(f"[bench] selection: candidate {best} of {len(res)}, speedup {out['standalone_speedup']}")
+    del S, flush
+    torch.cuda.empty_cache()
+    return out
 
 
 def run_gpu(workload: str, dtype: str, steps: int, warmup: int, variant: int, eq3_flush: bool = True):
@@ -462,6 +492,7 @@ def main():
             "kernel_config": sec["config"], "eq3": sec["eq3"],
         }
     copy = probe_copy() if args.probe_copy else None
+    selection = select_round(args.workload, args.dtype) if args.select else None
     w = prim["w"]
     desc = OPS[w.op][2]
     metric = (HEADLINE_METRIC if args.workload == HEADLINE and args.dtype == "f32"
@@ -494,6 +525,7 @@ def main():
             {"kernel": k["kernel"], "ms": round(k["ms"], 5), "alg_bytes": k["alg_bytes"],
              "gbs": round(k["gbs"], 1), "frac": round(k["gbs"] / PEAK_GBS, 4)} for k in prim["per_kernel"]],
         "eq3": prim["eq3"],
+        "selection": selection,
         "cpu_baseline": cpu,
         "fe_error_vs_oracle": fe,
         "secondary": secondary,
