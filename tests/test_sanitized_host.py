@@ -39,4 +39,6 @@ def test_sanitizer_setup_catches_a_planted_overflow(tmp_path):
                     str(src), "-o", exe], check=True, capture_output=True, text=True, timeout=120)
     env = dict(os.environ, ASAN_OPTIONS="abort_on_error=0:verify_asan_link_order=0")
     r = subprocess.run([exe], capture_output=True, text=True, timeout=120, env=env)
-    assert r.returncode != 0 and "heap-buffer-overflow" in r.stderr
+    # UBSan's object-size check or ASan's shadow check, whichever reports first
+    assert r.returncode != 0
+    assert "heap-buffer-overflow" in r.stderr or "insufficient space" in r.stderr, r.stderr
