@@ -11,9 +11,10 @@ device synchronizations.  One JSON line is printed:
 * value        -- whole-step throughput: algorithmic bytes (every input once,
                   every output once) per second
 * roofline     -- the dominant kernel's algorithmic bytes per launch divided by
-                  its average duration, from event pairs stamped by each launch
-                  of the timed region on the kernel's own stream; traffic is
-                  the calibrated rocprofv3 HBM byte count per launch
+                  its average duration, from event pairs stamped by the
+                  launches of every 8th step of the timed region, on the
+                  kernel's own stream; traffic is the calibrated rocprofv3 HBM
+                  byte count per launch
 * eq3          -- the MEP timing rule of Eq. 3 on the GPU: 3 warm-up calls,
                   R = 30 samples, each after a 1 GiB cache flush, trimmed
                   mean with the k = 3 fastest and slowest dropped
@@ -265,6 +266,9 @@ def select_round(workload: str, dtype: str):
     return out
 
 
+PROFILE_EVERY = 8
+
+
 def run_gpu(workload: str, dtype: str, steps: int, warmup: int, variant: int, eq3_flush: bool = True):
     import torch
 
@@ -277,7 +281,12 @@ def run_gpu(workload: str, dtype: str, steps: int, warmup: int, variant: int, eq
     for _ in range(warmup):
         S["step"]()
     torch.cuda.synchronize()
-    mep.mep_profile_begin(steps * len(S["kernels"]))
+    # stamp every PROFILE_EVERY-th step (all of its streaming launches): an
+    # event pair costs ~16 us of host time per launch, which would make small
+    # workloads host-bound and adds ~1 us to a headline step
+    nk = len(S["kernels"])
+    stamped = (steps + PROFILE_EVERY - 1) // PROFILE_EVERY
+    mep.mep_profile_begin_sampled(stamped * nk, nk, PROFILE_EVERY)
     log(f"[bench] timing {steps} steps")
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -286,16 +295,16 @@ def run_gpu(workload: str, dtype: str, steps: int, warmup: int, variant: int, eq
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     kern = S["kernels"]
-    samples, kern_ms, launches = mep.mep_profile_end_samples(steps * len(kern) + 16)
+    samples, kern_ms, launches = mep.mep_profile_end_samples(stamped * len(kern) + 16)
     config = mep.mep_variant_info(code, mep.dtype_code(S["tdt"]), S["m"], S["n"], max(variant, 0))
     ms_step = elapsed * 1e3 / steps
     eq3 = eq3_timing(S, ms_step) if eq3_flush else None
     mep.mep_set_variant(code, -1)
     per_kernel = []
-    if launches == steps * len(kern):
-        # launch position p of every step is the same kernel
+    if launches == stamped * len(kern):
+        # launch position p of every stamped step is the same kernel
         for p, (name, nbytes) in enumerate(kern):
-            ms = sum(samples[p::len(kern)]) / steps
+            ms = sum(samples[p::len(kern)]) / stamped
             per_kernel.append({"kernel": name, "ms": ms, "alg_bytes": nbytes,
                                "gbs": nbytes / (ms * 1e-3) / 1e9})
         dom = max(per_kernel, key=lambda k: k["ms"])

@@ -271,6 +271,15 @@ int mep_select_variant(const mep_call_t* call, int warmup, int R, int k, int inn
  * recorded launches and their summed duration, and disarms.  Not thread-safe.
  */
 int mep_profile_begin(int capacity);
+/* As mep_profile_begin, but stamps only a sample of the launches: counting
+ * the streaming-kernel launches from the call on (0, 1, 2, ...), launch i is
+ * recorded when (i / group) % every == 0, i.e. the first `group` launches of
+ * every `every` groups (group = the launches of one operation, so that
+ * GEMVER's two passes stay paired).  Stamping a launch costs host time and a
+ * little device time; sampling keeps that out of a timed loop.
+ * mep_profile_begin(cap) is mep_profile_begin_sampled(cap, 1, 1).  MEP_EINVAL
+ * for capacity, group or every below 1, or when already armed. */
+int mep_profile_begin_sampled(int capacity, int group, int every);
 int mep_profile_end(double* total_ms, int* launches);
 /* As mep_profile_end, but also returns each recorded launch's duration in
  * launch order (up to cap entries; operations with two streaming passes, such

@@ -389,6 +389,9 @@ static int check_ws(void* ws, size_t ws_bytes, size_t need)
 struct Prof {
     bool armed = false;
     int cap = 0, used = 0;
+    // launch ordinal since arming; launch i is stamped when (i / group) % every == 0
+    int64_t seen = 0;
+    int group = 1, every = 1;
     std::vector<hipEvent_t> start, stop;
 };
 static Prof g_prof;
@@ -396,7 +399,10 @@ static Prof g_prof;
 // The event pair for the next streaming launch while profiling is armed.
 static LaunchEvents prof_next()
 {
-    if (g_prof.armed && g_prof.used < g_prof.cap) {
+    if (!g_prof.armed)
+        return LaunchEvents{nullptr, nullptr};
+    const int64_t i = g_prof.seen++;
+    if ((i / g_prof.group) % g_prof.every == 0 && g_prof.used < g_prof.cap) {
         const LaunchEvents ev{g_prof.start[g_prof.used], g_prof.stop[g_prof.used]};
         ++g_prof.used;
         return ev;
@@ -1208,8 +1214,15 @@ int mep_check_fe(int dtype, const void* out, const double* ref, int64_t len, dou
 
 int mep_profile_begin(int capacity)
 {
+    return mep_profile_begin_sampled(capacity, 1, 1);
+}
+
+int mep_profile_begin_sampled(int capacity, int group, int every)
+{
     if (capacity < 1)
         return fail(MEP_EINVAL, "capacity must be >= 1");
+    if (group < 1 || every < 1)
+        return fail(MEP_EINVAL, "group and every must be >= 1");
     if (g_prof.armed)
         return fail(MEP_EINVAL, "profiling is already armed");
     g_prof.start.assign((size_t)capacity, nullptr);
@@ -1234,6 +1247,9 @@ int mep_profile_begin(int capacity)
     }
     g_prof.cap = capacity;
     g_prof.used = 0;
+    g_prof.seen = 0;
+    g_prof.group = group;
+    g_prof.every = every;
     g_prof.armed = true;
     return MEP_OK;
 }

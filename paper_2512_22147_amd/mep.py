@@ -30,7 +30,7 @@ EXPORTS = (
     "mep_run", "mep_time_trimmed", "mep_trimmed_mean", "mep_check_fe",
     "mep_variant_count", "mep_set_variant", "mep_variant_info", "mep_profile_begin", "mep_profile_end",
     "mep_stream_copy", "mep_last_error", "mep_version", "mep_select_variant",
-    "mep_reduce_sum", "mep_vector_add", "mep_gemver", "mep_profile_end_samples",
+    "mep_reduce_sum", "mep_vector_add", "mep_gemver", "mep_profile_end_samples", "mep_profile_begin_sampled",
 )
 
 
@@ -92,6 +92,7 @@ def lib() -> ctypes.CDLL:
     L.mep_set_variant.argtypes = [i, i]
     L.mep_variant_info.argtypes = [i, i, i64, i64, i, ctypes.c_char_p, sz]
     L.mep_profile_begin.argtypes = [i]
+    L.mep_profile_begin_sampled.argtypes = [i, i, i]
     L.mep_profile_end.argtypes = [ctypes.POINTER(d), ctypes.POINTER(ctypes.c_int)]
     L.mep_stream_copy.argtypes = [vp, vp, sz, vp]
     L.mep_reduce_sum.argtypes = [i, i64, vp, vp, vp, sz, vp]
@@ -367,6 +368,11 @@ def mep_set_variant(op: int, variant: int) -> None:
 
 def mep_profile_begin(capacity: int) -> None:
     _check(lib().mep_profile_begin(capacity))
+
+
+def mep_profile_begin_sampled(capacity: int, group: int, every: int) -> None:
+    """Stamp launch i (counted from here) when (i // group) % every == 0."""
+    _check(lib().mep_profile_begin_sampled(capacity, group, every))
 
 
 def mep_profile_end():

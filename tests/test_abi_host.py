@@ -32,7 +32,7 @@ def L():
 
 def test_library_exports_every_declared_function(L):
     names = declared_functions()
-    assert len(names) == 22
+    assert len(names) == 23
     for name in names:
         assert hasattr(L, name), f"{name} not exported"
     assert sorted(mep.EXPORTS) == names
@@ -239,6 +239,9 @@ def test_harness_errors(L):
     assert L.mep_run(ctypes.byref(c)) == mep.MEP_EINVAL
     assert L.mep_set_variant(17, 0) == mep.MEP_EINVAL
     assert L.mep_profile_begin(0) == mep.MEP_EINVAL
+    assert L.mep_profile_begin_sampled(4, 0, 1) == mep.MEP_EINVAL
+    assert L.mep_profile_begin_sampled(4, 1, 0) == mep.MEP_EINVAL
+    assert L.mep_profile_begin_sampled(0, 1, 1) == mep.MEP_EINVAL
     assert L.mep_profile_end(None, None) == mep.MEP_EINVAL
     assert L.mep_stream_copy(FAKE, FAKE * 2, 24, None) == mep.MEP_EALIGN
     assert L.mep_stream_copy(FAKE, FAKE + 16, 64, None) == mep.MEP_EINVAL

@@ -246,6 +246,13 @@ def test_harness_on_gpu():
     samples, tot, cnt = mep.mep_profile_end_samples(8)
     assert cnt == 6 and len(samples) == 6 and all(t > 0 for t in samples)
     assert tot == pytest.approx(sum(samples), rel=1e-9)
+    # sampled stamping: groups of GEMVER's two launches, every third group
+    # (7 calls = 14 launches -> launches 0, 1, 6, 7, 12, 13)
+    mep.mep_profile_begin_sampled(16, 2, 3)
+    for _ in range(7):
+        mep.mep_run(g)
+    samples, tot, cnt = mep.mep_profile_end_samples(16)
+    assert cnt == 6 and len(samples) == 6 and all(t > 0 for t in samples)
     mep.mep_profile_begin(4)
     with pytest.raises(mep.MepError):
         mep.mep_profile_end_samples(-1)
