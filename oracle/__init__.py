@@ -19,10 +19,10 @@ Contents
 * ``trimmed_mean``: Eq. 3 of Sec. 3.2 -- sort the R samples ascending, drop the
   k lowest and k highest, average the remaining R - 2k; only defined for
   R > 2k.
-* ``fe_error`` / ``fe_pass``: the functional-equivalence test of Eq. 4 under
-  this build's reading of the paper's requirement that outputs agree: the normwise relative error
-  max_i |out_i - ref_i| / max_i |ref_i|; any non-finite output fails; an
-  all-zero reference demands an all-zero output.
+* ``fe_error`` / ``fe_pass``: the functional-equivalence test of Eq. 4.  The
+  paper only asks that outputs agree; the metric taken for that is the
+  normwise relative error max_i |out_i - ref_i| / max_i |ref_i|; any
+  non-finite output fails; an all-zero reference demands an all-zero output.
 * ``select_next`` : Eqs. 4-5 -- among the candidates that pass FE, the one with
   the smallest trimmed-mean time becomes the next baseline.
 """
