@@ -380,3 +380,27 @@ def test_narrow_outputs_split_reduce(op, shape, dt):
         for k in ref:
             assert runs[0][k].tobytes() == runs[1][k].tobytes() == runs[2][k].tobytes(), \
                 f"{op} {k} candidate {v} differs between runs"
+
+
+# One shape per range of the default-shape rule (rows of 513-8193 vectors,
+# both sides of every split point), with enough rows that every workgroup
+# loops over several batches: the defaults of every op against the oracle.
+DEFAULT_RULE_SHAPES = [(2600, 2052), (1800, 3072), (1800, 3076), (1400, 4100), (1000, 6148),
+                       (800, 8196), (500, 12292), (400, 16388), (300, 24580)]
+
+
+@pytest.mark.parametrize("op", OPS)
+@pytest.mark.parametrize("shape", DEFAULT_RULE_SHAPES, ids=lambda s: f"{s[0]}x{s[1]}")
+def test_default_shapes_across_row_lengths(op, shape):
+    from paper_2512_22147_amd import mep
+
+    m, n = shape
+    for dt in DTYPES:
+        if dt == np.float64 and n % 2:
+            continue
+        ins = make_inputs(op, m, n, dt, seed=5000 + m + n)
+        ref = oracle_outputs(op, ins, dt)
+        code = op_code(op)
+        info = mep.mep_variant_info(code, mep.MEP_F32 if dt == np.float32 else mep.MEP_F64, m, n, 0)
+        got = gpu_outputs(op, ins, dt)
+        assert_parity(op, got, ref, dt, what=f"{m}x{n} default ({info})")
