@@ -127,10 +127,11 @@ int mep_gemver(int dtype, int64_t m, int64_t n, double alpha, double beta, const
 
 /*
  * s = sum_{i<n} x_i: the "reduction" sample of the AMD APP SDK table (Table 3,
- * Sec. 4.3).  x: n elements; s: one element of device memory.  Workgroups add
- * grid-strided shares into partials in ws (mep_workspace_bytes(
- * MEP_OP_REDUCE_SUM, dtype, 1, n) bytes), which one more kernel adds in a
- * fixed order: the result is reproducible and no atomics are used.
+ * Sec. 4.3).  x: n elements; s: one element of device memory.  Each workgroup
+ * adds one contiguous chunk of x into its partial in ws (mep_workspace_bytes(
+ * MEP_OP_REDUCE_SUM, dtype, 1, n) bytes), and one more kernel adds the
+ * partials in a fixed order: the result is reproducible and no atomics are
+ * used.
  * n = 0 gives s = 0.
  */
 int mep_reduce_sum(int dtype, int64_t n, const void* x, void* s, void* ws, size_t ws_bytes,
