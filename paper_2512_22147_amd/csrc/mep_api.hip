@@ -67,11 +67,20 @@ static Cfg preferred_shape(int mode, int esize, int64_t m, int64_t n, int64_t nv
     const int64_t mats = two ? 2 : 1;
     const bool stream = mats * m * n * esize > (int64_t(128) << 20);
     const int aux = stream ? 2 : 0;
+    // rows of <= 8 vectors: as many lanes per row as the row has vectors
+    // (2, 4 or 8; a wider group leaves most lanes idle: 2.4-4.3 instead of
+    // 5.7-6.6 TB/s for 1 GiB of 12- and 16-element fp32 rows)
+    if (nv <= 8)
+        return Cfg{nv <= 2 ? 2 : (nv <= 4 ? 4 : 8), 1, 8, 4, aux};
     // rows of <= 16 vectors: 16 compute units per XCD (512 workgroups) halve
     // the partial rows the single-workgroup column reduce adds (the step is
-    // ~4% faster for 2^20 x 64, the streaming kernel ~2% slower)
-    if (nv <= 16)
+    // ~4% faster for 2^20 x 64, the streaming kernel ~2% slower); fp64 BICG
+    // takes 4-row batches, which do not spill (5.6 instead of 3.4 TB/s)
+    if (nv <= 16) {
+        if (mode == MODE_BICG && esize == 8)
+            return Cfg{16, 1, 4, 4, 2};
         return Cfg{16, 1, 8, 4, aux, 0, stream ? 16 : kCusPerXcd};
+    }
     if (nv <= 64)
         return Cfg{64, 1, 8, 4, aux};
     if (nv <= 256)

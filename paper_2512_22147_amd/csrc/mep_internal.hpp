@@ -30,9 +30,14 @@ constexpr int kCusPerXcd = 32;
 // Vector path (16-byte loads), ordered by row capacity G * V; among equal
 // capacities the preferred shape comes first (measured on MI355X: streaming
 // the matrix with non-temporal loads is faster for every shape).
-constexpr int kNumVecCfg = 44;
+constexpr int kNumVecCfg = 51;
 constexpr Cfg kVecCfg[kNumVecCfg] = {
+    // rows of 1-8 vectors: 2, 4 or 8 lanes per row, 32, 16 or 8 rows per wave
+    {2, 1, 8, 4, 2},     {2, 1, 8, 4, 0},
+    {4, 1, 8, 4, 2},     {4, 1, 8, 4, 0},
+    {8, 1, 8, 4, 2},     {8, 1, 8, 4, 0},
     {16, 1, 8, 4, 2},    {16, 1, 8, 4, 2, 0, 24}, {16, 1, 8, 4, 2, 0, 16}, {16, 1, 8, 4, 0},
+    {16, 1, 4, 4, 2},
     {64, 1, 8, 4, 2},    {64, 1, 8, 4, 0},
     {64, 2, 4, 4, 2},    {64, 2, 4, 4, 0},    {64, 4, 2, 4, 2},    {64, 4, 2, 4, 0},
     // 512 vectors

@@ -33,7 +33,9 @@ def _gpu():
 # shapes chosen to cover every row-group width, ragged tails of rows and of
 # row vectors, several workgroups and several tiles
 EDGE_SHAPES = [(1, 1), (1, 7), (7, 1), (3, 5), (63, 63), (64, 64), (65, 129), (100, 1000),
-               (257, 4100), (1000, 1024), (37, 16388), (300, 8192), (129, 16384)]
+               (257, 4100), (1000, 1024), (37, 16388), (300, 8192), (129, 16384),
+               # rows of 1-8 vectors (2-, 4- and 8-lane row groups), ragged row counts
+               (1001, 4), (777, 8), (1000, 12), (513, 16), (299, 32)]
 
 
 @pytest.mark.parametrize("dt", DTYPES, ids=["f32", "f64"])
@@ -56,7 +58,7 @@ def test_edge_shapes_every_candidate(op, shape, dt):
 
 @pytest.mark.parametrize("dt", DTYPES, ids=["f32", "f64"])
 @pytest.mark.parametrize("op", OPS)
-@pytest.mark.parametrize("shape", [(2048, 4096), (513, 1027), (4000, 64), (3, 40000)],
+@pytest.mark.parametrize("shape", [(2048, 4096), (513, 1027), (4000, 64), (3, 40000), (5001, 8), (3000, 12)],
                          ids=lambda s: f"{s[0]}x{s[1]}")
 def test_integer_inputs_bit_exact(op, shape, dt):
     """Entries in {-1, 0, 1}: every partial sum is an integer below 2^24, so
@@ -382,10 +384,11 @@ def test_narrow_outputs_split_reduce(op, shape, dt):
                 f"{op} {k} candidate {v} differs between runs"
 
 
-# One shape per range of the default-shape rule (rows of 513-8193 vectors,
+# One shape per range of the default-shape rule (rows of 1-8193 vectors,
 # both sides of every split point), with enough rows that every workgroup
 # loops over several batches: the defaults of every op against the oracle.
-DEFAULT_RULE_SHAPES = [(2600, 2052), (1800, 3072), (1800, 3076), (1400, 4100), (1000, 6148),
+DEFAULT_RULE_SHAPES = [(100003, 4), (60001, 8), (40000, 12), (30001, 16), (20000, 32),
+                       (2600, 2052), (1800, 3072), (1800, 3076), (1400, 4100), (1000, 6148),
                        (800, 8196), (500, 12292), (400, 16388), (300, 24580)]
 
 
