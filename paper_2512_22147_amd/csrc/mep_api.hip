@@ -83,6 +83,8 @@ static Cfg preferred_shape(int mode, int esize, int64_t m, int64_t n, int64_t nv
     }
     if (nv <= 64)
         return Cfg{64, 1, 8, 4, aux};
+    if (nv <= 128 && (mode == MODE_MV || mode == MODE_BICG || (mode & F_TWO)))
+        return Cfg{64, 2, 4, 4, aux};  // 4-11% faster than 64 x 4 x 2 for these at 128 vectors
     if (nv <= 256)
         return Cfg{64, 4, 2, 4, aux};
     // the rank-2 update that stores Ahat (GEMVER's first pass): 512-lane groups
