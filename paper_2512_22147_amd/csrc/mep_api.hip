@@ -149,6 +149,27 @@ static Cfg preferred_shape(int mode, int esize, int64_t m, int64_t n, int64_t nv
     return Cfg{512, 16, 1, 2, laux, 0, stream && full ? 26 : kCusPerXcd};
 }
 
+// The default of the element-wise path: the narrowest row group that holds
+// the row, with 16 elements per lane in flight for fp32 and 8 for fp64 (64
+// bytes either way; deeper fp64 batches spill).
+static Cfg preferred_scalar_shape(int esize, int64_t n)
+{
+    const int per_lane = esize == 4 ? 16 : 8;
+    if (n <= 64) {
+        const int g = n <= 8 ? 8 : (n <= 16 ? 16 : (n <= 32 ? 32 : 64));
+        return Cfg{g, 1, per_lane, 4, 2};
+    }
+    if (n <= 128)
+        return Cfg{64, 2, per_lane / 2, 4, 2};
+    if (n <= 256)
+        return Cfg{64, 4, per_lane / 4, 4, 2};
+    if (n <= 512)
+        return Cfg{256, 2, per_lane / 2, 4, 2};
+    if (n <= 1024)
+        return Cfg{256, 4, per_lane / 4, 4, 2};
+    return Cfg{1024, 8, per_lane / 8, 4, 2};
+}
+
 static bool same_cfg(const Cfg& a, const Cfg& b)
 {
     return a.G == b.G && a.V == b.V && a.B == b.B && a.WPE == b.WPE && a.AUX == b.AUX && a.MAP == b.MAP &&
@@ -188,8 +209,8 @@ int stream_candidates(int esize, bool vec, int mode, int64_t m, int64_t n, int* 
                 idx[cnt++] = i;
     }
     // the measured default goes first when it is among the candidates
-    if (vec) {
-        const Cfg want = preferred_shape(mode, esize, m, n, nv);
+    {
+        const Cfg want = vec ? preferred_shape(mode, esize, m, n, nv) : preferred_scalar_shape(esize, n);
         for (int k = 1; k < cnt; ++k) {
             if (same_cfg(tab[idx[k]], want)) {
                 const int keep = idx[k];

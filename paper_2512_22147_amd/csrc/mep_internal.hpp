@@ -55,9 +55,17 @@ constexpr Cfg kVecCfg[kNumVecCfg] = {
     {512, 16, 1, 2, 2, 0, 26}, {512, 16, 1, 2, 2, 0, 24}, {512, 16, 1, 2, 2}, {512, 16, 1, 2, 2, 1},
     {1024, 8, 1, 4, 2},  {256, 32, 1, 1, 2},   {512, 16, 1, 2, 0},  {1024, 8, 1, 4, 0},
     {256, 32, 1, 1, 0}};
-// Element-wise path (rows not 16-byte aligned): one element per load.
-constexpr int kNumScalarCfg = 3;
-constexpr Cfg kScalarCfg[kNumScalarCfg] = {{64, 4, 2, 4, 2}, {256, 4, 2, 4, 2}, {1024, 8, 1, 4, 2}};
+// Element-wise path (rows not 16-byte aligned): one element per load, so
+// batches are deep (B * V = 8-16 elements per lane) to keep 32-64 bytes per
+// lane in flight; short rows get as many lanes as they have elements.
+// Ordered by row capacity G * V.
+constexpr int kNumScalarCfg = 16;
+constexpr Cfg kScalarCfg[kNumScalarCfg] = {
+    {8, 1, 16, 4, 2},   {8, 1, 8, 4, 2},    {16, 1, 16, 4, 2},  {16, 1, 8, 4, 2},
+    {32, 1, 16, 4, 2},  {32, 1, 8, 4, 2},   {64, 1, 16, 4, 2},  {64, 1, 8, 4, 2},
+    {64, 2, 8, 4, 2},   {64, 4, 4, 4, 2},   {64, 4, 2, 4, 2},
+    {256, 2, 8, 4, 2},  {256, 4, 4, 4, 2},  {256, 4, 2, 4, 2},
+    {1024, 8, 2, 4, 2}, {1024, 8, 1, 4, 2}};
 
 // Rows per batch an instance really uses: two-matrix modes (GESUMMV) hold
 // twice the rows in registers, so they take half the batch.

@@ -35,7 +35,9 @@ def _gpu():
 EDGE_SHAPES = [(1, 1), (1, 7), (7, 1), (3, 5), (63, 63), (64, 64), (65, 129), (100, 1000),
                (257, 4100), (1000, 1024), (37, 16388), (300, 8192), (129, 16384),
                # rows of 1-8 vectors (2-, 4- and 8-lane row groups), ragged row counts
-               (1001, 4), (777, 8), (1000, 12), (513, 16), (299, 32)]
+               (1001, 4), (777, 8), (1000, 12), (513, 16), (299, 32),
+               # short misaligned rows (element-wise path, 8-64-lane groups)
+               (1001, 7), (999, 33), (501, 101)]
 
 
 @pytest.mark.parametrize("dt", DTYPES, ids=["f32", "f64"])
@@ -388,6 +390,7 @@ def test_narrow_outputs_split_reduce(op, shape, dt):
 # both sides of every split point), with enough rows that every workgroup
 # loops over several batches: the defaults of every op against the oracle.
 DEFAULT_RULE_SHAPES = [(100003, 4), (60001, 8), (40000, 12), (30001, 16), (20000, 32),
+                       (50001, 7), (20001, 33), (10001, 101), (3001, 1001),
                        (2600, 2052), (1800, 3072), (1800, 3076), (1400, 4100), (1000, 6148),
                        (800, 8196), (500, 12292), (400, 16388), (300, 24580)]
 
