@@ -139,7 +139,7 @@ static Cfg preferred_shape(int mode, int esize, int64_t m, int64_t n, int64_t nv
     // compute unit.  Cached: y = A x and GESUMMV still read non-temporally
     // (~10% faster), the column-sum modes cached.
     const int laux = stream || !col ? 2 : 0;
-    const bool full = (nv > 3584 && nv <= 4096) || nv > 7168;
+    const bool full = (nv > 3584 && nv <= 4096) || (nv > 7168 && nv <= 8192);  // longer: column panels
     if (nv <= 4096 || two) {
         const int cux = !stream || !full ? kCusPerXcd
                         : two ? (nv <= 4096 ? 22 : kCusPerXcd)
@@ -241,7 +241,14 @@ Plan plan_stream(int esize, bool vec, int mode, int64_t m, int64_t n, int varian
     const int64_t nblk = (m + rows_per_block - 1) / rows_per_block;
     // enough workgroups to fill the shape's CUX compute units per XCD at its occupancy
     const int64_t per_cu = p.threads <= 256 ? 4 : (p.threads == 512 && p.c.WPE >= 4 ? 2 : 1);
-    p.nb = std::max<int64_t>(1, std::min<int64_t>(nblk, (int64_t)kXcds * p.c.CUX * per_cu));
+    int64_t fill = (int64_t)kXcds * p.c.CUX * per_cu;
+    // column sums over several panels: the panels already fill the chip, and
+    // every row workgroup adds a partial row of n to the workspace (208
+    // partial rows for 268 matrix rows of 10^6 elements would cost as much
+    // traffic as the matrix), so the workgroups of a panel share the chip
+    if ((mode & F_COL) && p.panels > 1)
+        fill = std::max<int64_t>(1, (fill + p.panels - 1) / p.panels);
+    p.nb = std::max<int64_t>(1, std::min<int64_t>(nblk, fill));
     return p;
 }
 
