@@ -24,7 +24,10 @@
  * - 0 <= m <= 2^30 and 0 <= n <= 65535 * 8192.  A zero-length vector may be NULL.  An empty sum is
  *   zero: e.g. with n = 0, y = A x is all zeros.
  * - stream is a hipStream_t (NULL = the default stream).  Operations only
- *   enqueue work and return; they never synchronize.
+ *   enqueue kernels and return: they never synchronize, allocate or issue a
+ *   memset, so a caller may capture them into a HIP graph (outside
+ *   mep_profile_begin ... mep_profile_end, whose event stamps are not meant
+ *   for capture).
  * - ws is a caller-owned device workspace of at least
  *   mep_workspace_bytes(op, dtype, m, n) bytes (may be NULL when that is 0).
  *   Its contents on entry are irrelevant and on exit unspecified.
