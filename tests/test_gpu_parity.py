@@ -410,3 +410,33 @@ def test_default_shapes_across_row_lengths(op, shape):
         info = mep.mep_variant_info(code, mep.MEP_F32 if dt == np.float32 else mep.MEP_F64, m, n, 0)
         got = gpu_outputs(op, ins, dt)
         assert_parity(op, got, ref, dt, what=f"{m}x{n} default ({info})")
+
+
+def _random_cases(count=72, seed=2026):
+    """Seeded random shapes over the whole planning space: row lengths from 1
+    to ~70000 elements (narrow groups, vector and element-wise paths, column
+    panels), 1 to ~20000 rows, every op and both dtypes; sized so that the
+    oracle finishes each in well under a second."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    while len(cases) < count:
+        n = int(np.exp(rng.uniform(0, np.log(70000))))
+        m = int(np.exp(rng.uniform(0, np.log(20000))))
+        if m * n > 6_000_000:
+            continue
+        op = OPS[int(rng.integers(len(OPS)))]
+        dt = DTYPES[int(rng.integers(2))]
+        cases.append((op, m, n, dt))
+    return cases
+
+
+RANDOM_CASES = _random_cases()
+
+
+@pytest.mark.parametrize("case", range(len(RANDOM_CASES)))
+def test_random_shapes(case):
+    op, m, n, dt = RANDOM_CASES[case]
+    ins = make_inputs(op, m, n, dt, seed=7000 + case)
+    ref = oracle_outputs(op, ins, dt)
+    got = gpu_outputs(op, ins, dt)
+    assert_parity(op, got, ref, dt, what=f"case {case}: {op} {m}x{n} {np.dtype(dt).name}")
