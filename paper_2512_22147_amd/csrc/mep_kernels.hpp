@@ -595,8 +595,16 @@ k_stream(StreamArgs<T> a)
 #pragma unroll
             for (int v = 0; v < V; ++v) {
                 const int64_t c = (int64_t)(v * G + g) * VW;
-                if (c < pcols)
-                    store_vec_nt<T, VW>(out + c, acc[v]);
+                // fp32: written through (5% off the cache-resident BICG 4096^2
+                // step); fp64 keeps non-temporal stores, with which the
+                // 16384-wide kernel's registers fit (write-through: 20% slower)
+                if (c < pcols) {
+                    if constexpr (sizeof(T) == 4)
+                        store_buf<T, VW, kWriteThrough>(acc[v], make_rsrc(out, (uint32_t)(pcols * sizeof(T))),
+                                                        (uint32_t)(c * sizeof(T)));
+                    else
+                        store_vec_nt<T, VW>(out + c, acc[v]);
+                }
             }
         } else {
             // row groups of one wave first (butterfly over the lane bits above G) ...
@@ -624,9 +632,7 @@ k_stream(StreamArgs<T> a)
                 for (int w = 1; w < NWAVES; ++w)
                     t += cred[(w * G + gg) * V + vv];
                 const int64_t c = (int64_t)(vv * G + gg) * VW;
-                // written through: 2.3% off a 2^20 x 64 A^T w step (non-temporal
-                // stores stay on the one-row-group path above, where write-through
-                // stores made the fp64 16384-wide kernel 20% slower)
+                // written through: 2.3% off a 2^20 x 64 A^T w step
                 if (c < pcols)
                     store_buf<T, VW, kWriteThrough>(t, make_rsrc(out, (uint32_t)(pcols * sizeof(T))),
                                                     (uint32_t)(c * sizeof(T)));
