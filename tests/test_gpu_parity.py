@@ -36,6 +36,8 @@ EDGE_SHAPES = [(1, 1), (1, 7), (7, 1), (3, 5), (63, 63), (64, 64), (65, 129), (1
                (257, 4100), (1000, 1024), (37, 16388), (300, 8192), (129, 16384),
                # rows of 1-8 vectors (2-, 4- and 8-lane row groups), ragged row counts
                (1001, 4), (777, 8), (1000, 12), (513, 16), (299, 32),
+               # 16-lane row groups in workgroups of 256 and 1024 threads
+               (1500, 60), (3001, 64),
                # short misaligned rows (element-wise path, 8-64-lane groups)
                (1001, 7), (999, 33), (501, 101)]
 
