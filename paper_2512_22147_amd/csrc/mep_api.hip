@@ -224,15 +224,13 @@ int stream_candidates(int esize, bool vec, int mode, int64_t m, int64_t n, int* 
     return cnt;
 }
 
-Plan plan_stream(int esize, bool vec, int mode, int64_t m, int64_t n, int variant)
+// The plan of table shape `cfg` for an m x n matrix.
+static Plan plan_of(int esize, bool vec, int mode, int64_t m, int64_t n, int cfg)
 {
-    int idx[16];
-    const int cnt = stream_candidates(esize, vec, mode, m, n, idx);
-    const int k = (variant >= 0 && variant < cnt) ? variant : 0;
     Plan p;
     p.vec = vec;
     p.vw = vec ? 16 / esize : 1;
-    p.cfg = idx[k];
+    p.cfg = cfg;
     p.c = vec ? kVecCfg[p.cfg] : kScalarCfg[p.cfg];
     p.threads = p.c.G < 256 ? 256 : p.c.G;
     p.pw = (int64_t)p.c.G * p.c.V * p.vw;
@@ -250,6 +248,14 @@ Plan plan_stream(int esize, bool vec, int mode, int64_t m, int64_t n, int varian
         fill = std::max<int64_t>(1, (fill + p.panels - 1) / p.panels);
     p.nb = std::max<int64_t>(1, std::min<int64_t>(nblk, fill));
     return p;
+}
+
+Plan plan_stream(int esize, bool vec, int mode, int64_t m, int64_t n, int variant)
+{
+    int idx[16];
+    const int cnt = stream_candidates(esize, vec, mode, m, n, idx);
+    const int k = (variant >= 0 && variant < cnt) ? variant : 0;
+    return plan_of(esize, vec, mode, m, n, idx[k]);
 }
 
 static std::atomic<int> g_variant[8] = {{-1}, {-1}, {-1}, {-1}, {-1}, {-1}, {-1}, {-1}};
@@ -306,7 +312,39 @@ static WsLayout layout_for(int mode, const Plan& p, int esize, int64_t m, int64_
 static bool vec_ok_n(int esize, int64_t n) { return n % (16 / esize) == 0; }
 static bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
-// Largest workspace over both load paths and every candidate shape.
+// Largest workspace of any candidate of `mode` on one load path.
+static size_t max_layout(int mode, int esize, bool vec, int64_t m, int64_t n)
+{
+    int idx[16];
+    const int cnt = stream_candidates(esize, vec, mode, m, n, idx);
+    size_t best = 0;
+    for (int k = 0; k < cnt; ++k)
+        best = std::max(best, layout_for(mode, plan_of(esize, vec, mode, m, n, idx[k]), esize, m, n, false).total);
+    return best;
+}
+
+// Two-pass ATAX (rows over column panels): A x over panels into t, then
+// A^T t; both passes take the same variant index (each list clipped to its
+// default), and the space of the partial dots, t and the column partials is
+// held at once.
+static size_t two_pass_ata_x_ws(int esize, bool vec, int64_t m, int64_t n)
+{
+    int i1[16], i2[16];
+    const int c1 = stream_candidates(esize, vec, MODE_MV, m, n, i1);
+    const int c2 = stream_candidates(esize, vec, MODE_ATW, m, n, i2);
+    size_t best = 0;
+    for (int k = 0; k < std::max(c1, c2); ++k) {
+        const WsLayout l1 = layout_for(MODE_MV, plan_of(esize, vec, MODE_MV, m, n, i1[k < c1 ? k : 0]), esize, m,
+                                       n, true);
+        const WsLayout l2 = layout_for(MODE_ATW, plan_of(esize, vec, MODE_ATW, m, n, i2[k < c2 ? k : 0]), esize,
+                                       m, n, false);
+        best = std::max(best, l1.dotpart + l1.tvec + l2.colpart);
+    }
+    return best;
+}
+
+// Largest workspace over both load paths and every candidate shape.  Each
+// candidate list is built once (this runs on every operation call).
 static size_t ws_bytes_mode(int mode, int esize, int64_t m, int64_t n)
 {
     if (m == 0 || n == 0)
@@ -316,38 +354,24 @@ static size_t ws_bytes_mode(int mode, int esize, int64_t m, int64_t n)
         const bool vec = v == 0;
         if (vec && !vec_ok_n(esize, n))
             continue;
-        int idx[16];
-        const int cnt = stream_candidates(esize, vec, mode, m, n, idx);
-        for (int k = 0; k < cnt; ++k) {
-            const Plan p = plan_stream(esize, vec, mode, m, n, k);
-            if (mode == MODE_GEMV1) {
-                // pass 1 column partials, then (reusing the space) pass 2 partial dots
-                size_t s2 = 0;
-                int i2[16];
-                const int c2 = stream_candidates(esize, vec, MODE_MV, m, n, i2);
-                for (int k2 = 0; k2 < c2; ++k2)
-                    s2 = std::max(s2, layout_for(MODE_MV, plan_stream(esize, vec, MODE_MV, m, n, k2), esize,
-                                                 m, n, false).total);
-                best = std::max(best, std::max(layout_for(mode, p, esize, m, n, false).total, s2));
-            } else if (mode == MODE_ATAX && p.panels > 1) {
-                // two passes: A x over panels, then A^T t over panels
-                size_t s = 0;
-                for (int k2 = 0; k2 < 16; ++k2) {
-                    int i1[16], i2[16];
-                    const int c1 = stream_candidates(esize, vec, MODE_MV, m, n, i1);
-                    const int c2 = stream_candidates(esize, vec, MODE_ATW, m, n, i2);
-                    if (k2 >= c1 && k2 >= c2)
-                        break;
-                    const Plan p1 = plan_stream(esize, vec, MODE_MV, m, n, k2 < c1 ? k2 : 0);
-                    const Plan p2 = plan_stream(esize, vec, MODE_ATW, m, n, k2 < c2 ? k2 : 0);
-                    const WsLayout l1 = layout_for(MODE_MV, p1, esize, m, n, true);
-                    const WsLayout l2 = layout_for(MODE_ATW, p2, esize, m, n, false);
-                    s = std::max(s, l1.dotpart + l1.tvec + l2.colpart);
-                }
-                best = std::max(best, s);
-            } else {
-                best = std::max(best, layout_for(mode, p, esize, m, n, false).total);
+        if (mode == MODE_GEMV1) {
+            // pass 1 column partials, then (reusing the space) pass 2 partial dots
+            best = std::max({best, max_layout(MODE_GEMV1, esize, vec, m, n), max_layout(MODE_MV, esize, vec, m, n)});
+        } else if (mode == MODE_ATAX) {
+            int idx[16];
+            const int cnt = stream_candidates(esize, vec, mode, m, n, idx);
+            bool two_pass = false;
+            for (int k = 0; k < cnt; ++k) {
+                const Plan p = plan_of(esize, vec, mode, m, n, idx[k]);
+                if (p.panels > 1)
+                    two_pass = true;
+                else
+                    best = std::max(best, layout_for(mode, p, esize, m, n, false).total);
             }
+            if (two_pass)
+                best = std::max(best, two_pass_ata_x_ws(esize, vec, m, n));
+        } else {
+            best = std::max(best, max_layout(mode, esize, vec, m, n));
         }
     }
     return best;
