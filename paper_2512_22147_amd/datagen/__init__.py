@@ -48,7 +48,7 @@ def _load():
         lib.mep_dg_bits.argtypes = [u64, u64, u64, i64, vp]
         for name in ("uniform", "normal", "ternary"):
             for t in ("f32", "f64"):
-                getattr(lib, f"mep_dg_{name}_{t}").argtypes = [u64, u64, i64, vp]
+                getattr(lib, f"mep_dg_{name}_{t}").argtypes = [u64, u64, u64, i64, vp]
         _lib = lib
     return _lib
 
@@ -60,7 +60,7 @@ def bits(seed: int, array_id: int, count: int, first: int = 0) -> np.ndarray:
     return out
 
 
-def _draw(kind: str, seed: int, array_id: int, shape, dtype) -> np.ndarray:
+def _draw(kind: str, seed: int, array_id: int, shape, dtype, first: int = 0) -> np.ndarray:
     dtype = np.dtype(dtype)
     if dtype == np.float32:
         suffix = "f32"
@@ -69,25 +69,29 @@ def _draw(kind: str, seed: int, array_id: int, shape, dtype) -> np.ndarray:
     else:
         raise ValueError(f"unsupported dtype {dtype}")
     out = np.empty(shape, dtype=dtype)
-    getattr(_load(), f"mep_dg_{kind}_{suffix}")(seed, array_id, out.size, out.ctypes.data)
+    if first < 0:
+        raise ValueError("first must be >= 0")
+    getattr(_load(), f"mep_dg_{kind}_{suffix}")(seed, array_id, first, out.size, out.ctypes.data)
     return out
 
 
-def uniform(seed: int, array_id: int, shape, dtype=np.float32) -> np.ndarray:
-    """i.i.d. uniform[-1, 1) values, exact in the element type."""
-    return _draw("uniform", seed, array_id, shape, dtype)
+def uniform(seed: int, array_id: int, shape, dtype=np.float32, first: int = 0) -> np.ndarray:
+    """i.i.d. uniform[-1, 1) values, exact in the element type.  ``first``:
+    counter of the first element, so that pieces of one large array can be
+    drawn one at a time (elements first, first + 1, ... of array array_id)."""
+    return _draw("uniform", seed, array_id, shape, dtype, first)
 
 
-def normal(seed: int, array_id: int, shape, dtype=np.float32) -> np.ndarray:
+def normal(seed: int, array_id: int, shape, dtype=np.float32, first: int = 0) -> np.ndarray:
     """i.i.d. normal(0, 1) values (Box-Muller in fp64, rounded to dtype)."""
-    return _draw("normal", seed, array_id, shape, dtype)
+    return _draw("normal", seed, array_id, shape, dtype, first)
 
 
-def ternary(seed: int, array_id: int, shape, dtype=np.float32) -> np.ndarray:
+def ternary(seed: int, array_id: int, shape, dtype=np.float32, first: int = 0) -> np.ndarray:
     """i.i.d. values in {-1, 0, 1}; every sum of products of them is an
     integer, so results are exact in any summation order while partial sums
     stay below 2^24 (fp32) or 2^53 (fp64)."""
-    return _draw("ternary", seed, array_id, shape, dtype)
+    return _draw("ternary", seed, array_id, shape, dtype, first)
 
 
 # ---------------------------------------------------------------------------

@@ -43,6 +43,9 @@ static uint64_t dg_key(uint64_t seed, uint64_t array_id)
     return dg_mix(seed + (array_id + 1) * DG_GAMMA);
 }
 
+/* Every draw below fills out[k] with element first + k of the array, so a
+ * large array can be drawn in pieces that match one whole draw bit for bit. */
+
 /* Raw 64-bit draws: out[k] = bits(seed, array_id, first + k). */
 void mep_dg_bits(uint64_t seed, uint64_t array_id, uint64_t first, int64_t count, uint64_t* out)
 {
@@ -52,23 +55,23 @@ void mep_dg_bits(uint64_t seed, uint64_t array_id, uint64_t first, int64_t count
         out[k] = dg_mix(key + (first + (uint64_t)k + 1) * DG_GAMMA);
 }
 
-void mep_dg_uniform_f32(uint64_t seed, uint64_t array_id, int64_t count, float* out)
+void mep_dg_uniform_f32(uint64_t seed, uint64_t array_id, uint64_t first, int64_t count, float* out)
 {
     const uint64_t key = dg_key(seed, array_id);
 #pragma omp parallel for schedule(static)
     for (int64_t k = 0; k < count; ++k) {
-        uint64_t b = dg_mix(key + ((uint64_t)k + 1) * DG_GAMMA);
+        uint64_t b = dg_mix(key + (first + (uint64_t)k + 1) * DG_GAMMA);
         int64_t v = (int64_t)(b >> 40) - (int64_t)(1LL << 23);
         out[k] = (float)v * 0x1p-23f;
     }
 }
 
-void mep_dg_uniform_f64(uint64_t seed, uint64_t array_id, int64_t count, double* out)
+void mep_dg_uniform_f64(uint64_t seed, uint64_t array_id, uint64_t first, int64_t count, double* out)
 {
     const uint64_t key = dg_key(seed, array_id);
 #pragma omp parallel for schedule(static)
     for (int64_t k = 0; k < count; ++k) {
-        uint64_t b = dg_mix(key + ((uint64_t)k + 1) * DG_GAMMA);
+        uint64_t b = dg_mix(key + (first + (uint64_t)k + 1) * DG_GAMMA);
         int64_t v = (int64_t)(b >> 11) - (int64_t)(1LL << 52);
         out[k] = (double)v * 0x1p-52;
     }
@@ -83,38 +86,38 @@ static double dg_normal(uint64_t key, int64_t k)
     return sqrt(-2.0 * log(u1)) * cos(6.283185307179586476925286766559 * u2);
 }
 
-void mep_dg_normal_f32(uint64_t seed, uint64_t array_id, int64_t count, float* out)
+void mep_dg_normal_f32(uint64_t seed, uint64_t array_id, uint64_t first, int64_t count, float* out)
 {
     const uint64_t key = dg_key(seed, array_id);
 #pragma omp parallel for schedule(static)
     for (int64_t k = 0; k < count; ++k)
-        out[k] = (float)dg_normal(key, k);
+        out[k] = (float)dg_normal(key, (int64_t)first + k);
 }
 
-void mep_dg_normal_f64(uint64_t seed, uint64_t array_id, int64_t count, double* out)
+void mep_dg_normal_f64(uint64_t seed, uint64_t array_id, uint64_t first, int64_t count, double* out)
 {
     const uint64_t key = dg_key(seed, array_id);
 #pragma omp parallel for schedule(static)
     for (int64_t k = 0; k < count; ++k)
-        out[k] = dg_normal(key, k);
+        out[k] = dg_normal(key, (int64_t)first + k);
 }
 
-void mep_dg_ternary_f32(uint64_t seed, uint64_t array_id, int64_t count, float* out)
+void mep_dg_ternary_f32(uint64_t seed, uint64_t array_id, uint64_t first, int64_t count, float* out)
 {
     const uint64_t key = dg_key(seed, array_id);
 #pragma omp parallel for schedule(static)
     for (int64_t k = 0; k < count; ++k) {
-        uint64_t b = dg_mix(key + ((uint64_t)k + 1) * DG_GAMMA);
+        uint64_t b = dg_mix(key + (first + (uint64_t)k + 1) * DG_GAMMA);
         out[k] = (float)((int)((b >> 32) % 3) - 1);
     }
 }
 
-void mep_dg_ternary_f64(uint64_t seed, uint64_t array_id, int64_t count, double* out)
+void mep_dg_ternary_f64(uint64_t seed, uint64_t array_id, uint64_t first, int64_t count, double* out)
 {
     const uint64_t key = dg_key(seed, array_id);
 #pragma omp parallel for schedule(static)
     for (int64_t k = 0; k < count; ++k) {
-        uint64_t b = dg_mix(key + ((uint64_t)k + 1) * DG_GAMMA);
+        uint64_t b = dg_mix(key + (first + (uint64_t)k + 1) * DG_GAMMA);
         out[k] = (double)((int)((b >> 32) % 3) - 1);
     }
 }

@@ -22,12 +22,12 @@ void oracle_gemver(int64_t m, int64_t n, double alpha, double beta, const double
                    const double* v1, const double* u2, const double* v2, const double* y, const double* z,
                    double* Ahat, double* x, double* w);
 void mep_dg_bits(uint64_t seed, uint64_t array_id, uint64_t first, int64_t count, uint64_t* out);
-void mep_dg_uniform_f32(uint64_t seed, uint64_t array_id, int64_t count, float* out);
-void mep_dg_uniform_f64(uint64_t seed, uint64_t array_id, int64_t count, double* out);
-void mep_dg_normal_f32(uint64_t seed, uint64_t array_id, int64_t count, float* out);
-void mep_dg_normal_f64(uint64_t seed, uint64_t array_id, int64_t count, double* out);
-void mep_dg_ternary_f32(uint64_t seed, uint64_t array_id, int64_t count, float* out);
-void mep_dg_ternary_f64(uint64_t seed, uint64_t array_id, int64_t count, double* out);
+void mep_dg_uniform_f32(uint64_t seed, uint64_t array_id, uint64_t first, int64_t count, float* out);
+void mep_dg_uniform_f64(uint64_t seed, uint64_t array_id, uint64_t first, int64_t count, double* out);
+void mep_dg_normal_f32(uint64_t seed, uint64_t array_id, uint64_t first, int64_t count, float* out);
+void mep_dg_normal_f64(uint64_t seed, uint64_t array_id, uint64_t first, int64_t count, double* out);
+void mep_dg_ternary_f32(uint64_t seed, uint64_t array_id, uint64_t first, int64_t count, float* out);
+void mep_dg_ternary_f64(uint64_t seed, uint64_t array_id, uint64_t first, int64_t count, double* out);
 
 static int failures = 0;
 #define CHECK(c, ...) do { if (!(c)) { fprintf(stderr, __VA_ARGS__); fputc('\n', stderr); ++failures; } } while (0)
@@ -40,16 +40,16 @@ static void shape(int64_t m, int64_t n, uint64_t seed)
     double *v1 = arr(n), *v2 = arr(n), *z = arr(n), *yv = arr(m);
     double *ym = arr(m), *zt = arr(n), *t = arr(m), *ya = arr(n), *q = arr(m), *s = arr(n), *g = arr(m);
     double *Ahat = arr(m * n), *xg = arr(n), *wg = arr(m);
-    mep_dg_uniform_f64(seed, 0, m * n, A);
-    mep_dg_normal_f64(seed, 1, m * n, B);
-    mep_dg_uniform_f64(seed, 2, n, x);
-    mep_dg_uniform_f64(seed, 3, m, w);
-    mep_dg_uniform_f64(seed, 4, m, u1);
-    mep_dg_uniform_f64(seed, 5, m, u2);
-    mep_dg_uniform_f64(seed, 6, n, v1);
-    mep_dg_uniform_f64(seed, 7, n, v2);
-    mep_dg_uniform_f64(seed, 8, n, z);
-    mep_dg_uniform_f64(seed, 9, m, yv);
+    mep_dg_uniform_f64(seed, 0, 0, m * n, A);
+    mep_dg_normal_f64(seed, 1, 0, m * n, B);
+    mep_dg_uniform_f64(seed, 2, 0, n, x);
+    mep_dg_uniform_f64(seed, 3, 0, m, w);
+    mep_dg_uniform_f64(seed, 4, 0, m, u1);
+    mep_dg_uniform_f64(seed, 5, 0, m, u2);
+    mep_dg_uniform_f64(seed, 6, 0, n, v1);
+    mep_dg_uniform_f64(seed, 7, 0, n, v2);
+    mep_dg_uniform_f64(seed, 8, 0, n, z);
+    mep_dg_uniform_f64(seed, 9, 0, m, yv);
 
     oracle_matvec(m, n, A, x, ym);
     oracle_matvec_t(m, n, A, w, zt);
@@ -100,17 +100,27 @@ static void generator(void)
     for (int64_t k = 0; k + 10 < n; ++k) CHECK(b1[k + 10] == b2[k], "counter form at %lld", (long long)k);
     float* f = (float*)malloc(n * sizeof(float));
     double* d = arr(n);
-    mep_dg_uniform_f32(1, 0, n, f);
+    mep_dg_uniform_f32(1, 0, 0, n, f);
     for (int64_t k = 0; k < n; ++k) CHECK(f[k] >= -1.0f && f[k] < 1.0f, "uniform f32 range");
-    mep_dg_uniform_f64(1, 0, n, d);
+    mep_dg_uniform_f64(1, 0, 0, n, d);
     for (int64_t k = 0; k < n; ++k) CHECK(d[k] >= -1.0 && d[k] < 1.0, "uniform f64 range");
-    mep_dg_normal_f32(1, 0, n, f);
-    mep_dg_normal_f64(1, 0, n, d);
+    mep_dg_normal_f32(1, 0, 0, n, f);
+    mep_dg_normal_f64(1, 0, 0, n, d);
     for (int64_t k = 0; k < n; ++k) CHECK(isfinite(f[k]) && isfinite(d[k]), "normal finite");
-    mep_dg_ternary_f32(1, 0, n, f);
-    mep_dg_ternary_f64(1, 0, n, d);
+    mep_dg_ternary_f32(1, 0, 0, n, f);
+    mep_dg_ternary_f64(1, 0, 0, n, d);
     for (int64_t k = 0; k < n; ++k) CHECK((f[k] == -1 || f[k] == 0 || f[k] == 1) && (d[k] == -1 || d[k] == 0 || d[k] == 1), "ternary");
-    mep_dg_uniform_f64(1, 0, 0, d);  /* empty draw writes nothing */
+    mep_dg_uniform_f64(1, 0, 0, 0, d);  /* empty draw writes nothing */
+    /* a draw from counter 10 on equals the tail of the draw from 0 */
+    double* d2 = arr(n);
+    mep_dg_uniform_f64(1, 0, 0, n, d);
+    mep_dg_uniform_f64(1, 0, 10, n - 10, d2);
+    for (int64_t k = 0; k + 10 < n; ++k) CHECK(d[k + 10] == d2[k], "uniform from counter 10 at %lld", (long long)k);
+    mep_dg_normal_f32(1, 0, 0, n, f);
+    float* f2 = (float*)malloc(n * sizeof(float));
+    mep_dg_normal_f32(1, 0, 10, n - 10, f2);
+    for (int64_t k = 0; k + 10 < n; ++k) CHECK(f[k + 10] == f2[k], "normal from counter 10 at %lld", (long long)k);
+    free(d2); free(f2);
     free(b1); free(b2); free(f); free(d);
 }
 

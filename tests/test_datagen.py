@@ -81,3 +81,17 @@ def test_workloads_sizes():
     ins = datagen.make_inputs("ata_x_1024")
     assert ins["A"].shape == (1024, 1024) and ins["x"].shape == (1024,)
     assert np.array_equal(ins["A"].ravel()[:8], datagen.uniform(0, 0, 8, np.float32))
+
+
+@pytest.mark.parametrize("kind", ["uniform", "normal", "ternary"])
+@pytest.mark.parametrize("dt", [np.float32, np.float64])
+def test_draws_in_pieces_equal_one_draw(kind, dt):
+    """A large array drawn piece by piece (each piece from its first element's
+    counter) is bit for bit the array drawn at once."""
+    draw = getattr(datagen, kind)
+    whole = draw(9, 4, (777, 41), dt)
+    cuts = [0, 1, 100, 101, 500, 777]
+    parts = [draw(9, 4, (b - a, 41), dt, first=a * 41) for a, b in zip(cuts[:-1], cuts[1:])]
+    assert np.array_equal(whole, np.concatenate(parts))
+    with pytest.raises(ValueError):
+        draw(9, 4, 3, dt, first=-1)
