@@ -248,7 +248,10 @@ int mep_variant_info(int op, int dtype, int64_t m, int64_t n, int variant, char*
  * previous setting is restored.  results (nullable, results_cap entries)
  * receives, per candidate, the trimmed mean (ms; NaN when not timed), the FE
  * error against the baseline (each output on its own scale, the worse of
- * the two) and the FE verdict.  A GEMVER call must be out of place (out2 !=
+ * the two) and the FE verdict.  With flush == 0 and a flush buffer in the
+ * call, the caches are cleared once (by writing the buffer) before each
+ * candidate runs, so that no candidate's warm timing inherits the cache
+ * state another one left behind.  A GEMVER call must be out of place (out2 !=
  * A), else MEP_EINVAL: each in-place run changes A.  The candidate set is fixed,
  * so one round is the whole search (the paper's D rounds regenerate
  * candidates; here nothing new appears in a later round).  Synchronizes

@@ -51,47 +51,63 @@ constexpr int64_t kMaxRow = int64_t(65535) * 8192;
 static int esize_of(int dtype) { return dtype == MEP_F32 ? 4 : (dtype == MEP_F64 ? 8 : 0); }
 
 // The default shape for a row of nv vectors, from candidate sweeps on MI355X
-// over row lengths of 512-8192 vectors, both element types, every operation,
-// and matrices that stay in the 256 MB Infinity Cache (32-64 MiB) or stream
-// from HBM (1 GiB).  What decides the shape is how much of each row group
-// holds data and how many bytes every compute unit keeps in flight: 512-lane
-// groups with batches of 4-8 rows win wherever a row is up to 2048 vectors,
-// and the 16384-element fp32 rows of the benchmark want 512 lanes x 8
-// vectors on 22-24 compute units per XCD.  Large matrices are streamed with
-// non-temporal loads; cache-resident ones mostly read faster cached, except
-// where a sweep showed otherwise (noted below).
+// (every operation, both element types, two boxes, rows of 1-8192 vectors,
+// matrices of 64 MiB that stay in the 256 MB Infinity Cache across calls and
+// of 1 GiB that stream from HBM).  What decides the shape is how much of each
+// row group holds data and how many bytes every compute unit keeps in
+// flight: the narrowest group that holds the row, except that rows filling
+// it (about 7/8 and more) often run faster on the next wider shape.
+// Non-temporal loads are the faster default for both matrix sizes (each
+// candidate timed after a 1 GiB write that clears the caches: a
+// non-temporal shape timed right after a cached-load one inherits its cache
+// state and reads 5-17% slower); the cache-resident exceptions are noted
+// where they are taken.
 static Cfg preferred_shape(int mode, int esize, int64_t m, int64_t n, int64_t nv)
 {
     const bool two = (mode & F_TWO) != 0;
     const bool col = (mode & F_COL) != 0;
+    const bool mv = mode == MODE_MV;
+    const bool atw = mode == MODE_ATW;
+    const bool bicg = mode == MODE_BICG;
+    const bool atax = (mode & F_FROMDOT) != 0;
     const int64_t mats = two ? 2 : 1;
     const bool stream = mats * m * n * esize > (int64_t(128) << 20);
-    const int aux = stream ? 2 : 0;
+    // load policy of rows of <= 256 vectors: non-temporal, except for
+    // GEMVER's first pass (it also stores Ahat) on a cache-resident matrix
+    const int naux = (mode & F_STORE) && !stream ? 0 : 2;
     // rows of <= 8 vectors: as many lanes per row as the row has vectors
     // (2, 4 or 8; a wider group leaves most lanes idle: 2.4-4.3 instead of
     // 5.7-6.6 TB/s for 1 GiB of 12- and 16-element fp32 rows)
-    if (nv <= 8)
-        return Cfg{nv <= 2 ? 2 : (nv <= 4 ? 4 : 8), 1, 8, 4, aux};
+    if (nv <= 8) {
+        // rows of one vector of a cache-resident matrix: cached loads (3-10%
+        // faster for y = A x, A^T w and BICG)
+        const int aux1 = nv == 1 && !stream && !atax && !two ? 0 : naux;
+        return Cfg{nv <= 2 ? 2 : (nv <= 4 ? 4 : 8), 1, 8, 4, aux1};
+    }
     // rows of <= 16 vectors: 16 compute units per XCD (512 workgroups) halve
     // the partial rows the single-workgroup column reduce adds (the step is
-    // ~4% faster for 2^20 x 64, the streaming kernel ~2% slower); fp64 BICG
-    // takes 4-row batches, which do not spill (5.6 instead of 3.4 TB/s)
-    if (nv <= 16) {
-        if (mode == MODE_BICG && esize == 8)
-            return Cfg{16, 1, 4, 4, 2};
-        return Cfg{16, 1, 8, 4, aux, 0, stream ? 16 : kCusPerXcd};
-    }
+    // ~4% faster for 2^20 x 64, the streaming kernel ~2% slower); BICG takes
+    // 4-row batches (fp64: 8-row batches spill, 5.6 instead of 3.4 TB/s)
+    if (nv <= 16)
+        return bicg ? Cfg{16, 1, 4, 4, 2} : Cfg{16, 1, 8, 4, naux, 0, 16};
     if (nv <= 64)
-        return Cfg{64, 1, 8, 4, aux};
-    if (nv <= 128 && (mode == MODE_MV || mode == MODE_BICG || (mode & F_TWO)))
-        return Cfg{64, 2, 4, 4, aux};  // 4-11% faster than 64 x 4 x 2 for these at 128 vectors
+        return Cfg{64, 1, 8, 4, naux};
+    // 65-128 vectors: 2 vectors per lane; A^T w and ATAX of streamed rows that
+    // fill them take 4 (half the rows per batch; 13-15% slower for 80-vector
+    // rows, a few % faster for 128), and so does GEMVER's first pass
+    if (nv <= 128) {
+        if ((mode & F_STORE) || ((atw || atax) && stream && nv > 112))
+            return Cfg{64, 4, 2, 4, naux};
+        return Cfg{64, 2, 4, 4, 2};
+    }
     if (nv <= 256)
-        return Cfg{64, 4, 2, 4, aux};
+        return Cfg{64, 4, 2, 4, naux};
     // the rank-2 update that stores Ahat (GEMVER's first pass): 512-lane groups
     // sized to the row up to 2048 vectors (fp64 rows of <= 512 vectors on
     // 256 x 4, where 512 x 2 x 8 spills), 1024-lane groups with 4 vectors per
     // lane beyond (panels past 4096 vectors)
     if (mode & F_STORE) {
+        const int aux = stream ? 2 : 0;
         if (nv <= 512)
             return stream && esize == 8 ? Cfg{256, 4, 2, 4, 2} : Cfg{512, 2, 8, 2, aux};
         if (nv <= 1024)
@@ -100,36 +116,56 @@ static Cfg preferred_shape(int mode, int esize, int64_t m, int64_t n, int64_t nv
             return stream ? Cfg{512, 8, 2, 2, 2} : Cfg{512, 4, 4, 2, 0};
         return Cfg{1024, 4, 2, 4, aux};
     }
-    const bool bicg64 = mode == MODE_BICG && esize == 8;  // the most registers per row
+    // 257-512 vectors: 512-vector shapes (the 1024-vector ones left a row of
+    // 320 vectors 15-30% slower): y = A x and GESUMMV of cache-resident
+    // matrices on 256-lane groups, the rest on 512 lanes x 1 vector with
+    // 8-row batches.  Rows past 3/4 of the group (y = A x: 7/8) go to the
+    // 1024-vector shapes; cache-resident ATAX and fp32 BICG only past 7/8,
+    // fp64 BICG (the most registers per row) never, and streamed fp64 BICG
+    // rows up to 3/4 run 2-12% faster on 256 x 2 x 4.
     if (nv <= 512) {
-        if (!stream)  // cached: y = A x and GESUMMV on 256-lane groups
-            return mode == MODE_MV || two ? Cfg{256, 2, 4, 4, 0} : Cfg{512, 2, 8, 2, 0};
-        if (bicg64)
+        if (bicg && esize == 8)
+            return stream && nv <= 384 ? Cfg{256, 2, 4, 4, 2} : Cfg{512, 1, 8, 4, 2};
+        if (!stream && (mv || two))
+            return Cfg{256, 2, 4, 4, 2};
+        if (nv <= 384 || (nv <= 448 && (mv || bicg || (atax && !stream))))
             return Cfg{512, 1, 8, 4, 2};
-        return mode == MODE_ATW || two ? Cfg{512, 2, 8, 2, 2} : Cfg{512, 2, 4, 4, 2};
+        if (atw || bicg || (atax && !stream) || (two && esize == 4))
+            return Cfg{512, 2, 8, 2, 2};
+        return Cfg{512, 2, 4, 4, 2};
     }
-    // Past 512 vectors a row group of 512 lanes takes V vectors per lane, V the
-    // power of two that makes 512 x V cover the row at least half full, and
-    // B = 16 / V rows per batch (the same vectors in flight whatever the row
-    // length).  Where the row fills more than 7/8 of that capacity, the sweeps
-    // found the next shape (the row twice over, half the rows per batch) a few
-    // % faster, and keep it there; lower in a range it leaves 3/4 of each
-    // group idle and runs up to 40% slower.
-    if (nv <= 896)
-        return two && !stream ? Cfg{256, 4, 2, 4, 2} : Cfg{512, 2, 8, 2, aux};
-    if (nv <= 1024) {  // non-temporal even where cached: measured faster
-        if (!stream && (mode == MODE_MV || two))
-            return Cfg{256, 4, 2, 4, 2};
-        return bicg64 && stream ? Cfg{512, 2, 8, 2, 2} : Cfg{512, 4, 4, 2, 2};
-    }
-    if (nv <= 1792)
-        return Cfg{512, 4, 4, 2, stream || !col ? 2 : 0};
-    if (nv <= 2048) {
+    // 513-1024 vectors: 512 lanes x 2 vectors, 8-row batches; y = A x and
+    // GESUMMV of cache-resident matrices on 256 x 4 (10-20% faster).
+    // Streamed rows that fill the group 7/8 or more run 3% faster on
+    // 512 x 4 x 4 (BICG: fp32 rows past 7/8 only).
+    if (nv <= 1024) {
         if (!stream)
-            return Cfg{512, 4, 4, 2, col ? 0 : 2};
-        if (mode == MODE_MV)
-            return Cfg{512, 8, 1, 4, 2};
-        return Cfg{512, 8, 2, 2, 2};  // every compute unit: the narrow grid is ~15% slower here
+            return mv || two ? Cfg{256, 4, 2, 4, 2} : Cfg{512, 2, 8, 2, 2};
+        if (bicg)
+            return esize == 4 && nv > 896 ? Cfg{512, 4, 4, 2, 2} : Cfg{512, 2, 8, 2, 2};
+        return nv >= 896 ? Cfg{512, 4, 4, 2, 2} : Cfg{512, 2, 8, 2, 2};
+    }
+    // 1025-2048 vectors: 512 lanes x 4 vectors, 4-row batches.  Streamed rows
+    // past ~13/16 of the group (y = A x: past ~11/16) run 2-6% faster on the
+    // 4096-vector shapes: 512 x 8 x 2, and for ATAX and BICG 1024-lane groups
+    // up to 15/16; y = A x of rows in the last 1/8 takes 1-row batches at 4
+    // waves per SIMD.  Cache-resident A^T w, and BICG and ATAX past ~13/16,
+    // read cached (the only place where cached loads are measurably faster).
+    if (nv <= 2048) {
+        if (!stream) {
+            if (mv || two)
+                return Cfg{512, 4, 4, 2, 2};
+            return Cfg{512, 4, 4, 2, atw || nv > 1664 ? 0 : 2};
+        }
+        if (mv)
+            return nv <= 1408 ? Cfg{512, 4, 4, 2, 2} : (nv <= 1792 ? Cfg{512, 8, 2, 2, 2} : Cfg{512, 8, 1, 4, 2});
+        if (nv <= 1664)
+            return Cfg{512, 4, 4, 2, 2};
+        if (nv <= 1920 && bicg)
+            return Cfg{1024, 2, 4, 4, 2};
+        if (nv <= 1920 && atax)
+            return Cfg{1024, 4, 2, 4, 2};
+        return Cfg{512, 8, 2, 2, 2};
     }
     // Longer rows.  Streamed rows that fill their group more than 7/8: one
     // matrix on 22 (ATAX) or 24 compute units per XCD for 4096-vector rows, 26
@@ -1213,6 +1249,9 @@ int mep_select_variant(const mep_call_t* call, int warmup, int R, int k, int inn
         return fail(MEP_EBUDGET, "Eq. 3 needs R > 2k >= 0, inner >= 1, warmup >= 0");
     if (call->op == MEP_OP_GEMVER && call->out2 == call->A && call->A != nullptr)
         return fail(MEP_EINVAL, "selection needs an out-of-place GEMVER call (each in-place run changes A)");
+    const bool have_flush = call->flush_buf != nullptr && call->flush_bytes > 0;
+    if (have_flush && (!aligned(call->flush_buf, 16) || call->flush_bytes % 16))
+        return fail(MEP_EALIGN, "flush buffer must be 16-byte aligned and a multiple of 16 bytes");
     const int count = mep_variant_count(call->op, call->dtype, call->m, call->n);
     if (count < 1)
         return fail(MEP_EINVAL, "no candidates for this call");
@@ -1224,6 +1263,18 @@ int mep_select_variant(const mep_call_t* call, int warmup, int R, int k, int inn
     for (int v = 0; v < count && rc == MEP_OK; ++v) {
         g_variant[call->op].store(v, std::memory_order_relaxed);
         mep_candidate_result_t r{std::numeric_limits<double>::quiet_NaN(), 0.0, 0};
+        // warm timings: no candidate may inherit the previous one's cache
+        // state (a non-temporal shape timed right after a cached-load one
+        // reads a cache-resident matrix 5-17% slower), so the caches are
+        // cleared once before each candidate runs
+        if (!flush && have_flush) {
+            const hipError_t fe = launch_flush(call->flush_buf, call->flush_bytes, 0x5BD1E995u + (uint32_t)v,
+                                               (hipStream_t)call->stream);
+            if (fe != hipSuccess) {
+                rc = hip_fail(fe, "flush");
+                break;
+            }
+        }
         rc = run_and_fetch(call, v == 0 ? base : out);
         if (rc)
             break;

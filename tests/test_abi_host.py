@@ -115,8 +115,8 @@ MEASURED_DEFAULTS = [
     # the benchmark workloads
     ("ATA_X", 0, 16384, 16384, "G=512 V=8 B=2 WPE=2 nt cyclic cus=22/32"),
     ("ATA_X", 1, 16384, 16384, "G=512 V=16 B=1 WPE=2 nt cyclic cus=26/32"),
-    ("ATA_X", 0, 1024, 1024, "G=64 V=4 B=2 WPE=4 cached"),
-    ("BICG", 0, 4096, 4096, "G=512 V=4 B=4 WPE=2 nt cyclic cus=32/32"),
+    ("ATA_X", 0, 1024, 1024, "G=64 V=4 B=2 WPE=4 nt"),
+    ("BICG", 0, 4096, 4096, "G=512 V=2 B=8 WPE=2 nt cyclic cus=32/32"),
     ("AXPBY_MV", 0, 8192, 8192, "G=512 V=8 B=1 WPE=2 nt cyclic cus=32/32"),
     ("MATVEC_T", 0, 1 << 20, 64, "G=16 V=1 B=8 WPE=4 nt cyclic cus=16/32"),
     ("GEMVER", 0, 16384, 16384, "G=1024 V=4 B=2 WPE=4 nt cyclic cus=32/32"),
@@ -142,11 +142,30 @@ MEASURED_DEFAULTS = [
     ("BICG", 0, 87267, 3076, "G=512 V=2 B=8 WPE=2 nt"),
     ("ATA_X", 0, 21838, 12292, "G=512 V=8 B=2 WPE=2 nt cyclic cus=32/32"),
     # cache-resident
-    ("MATVEC", 0, 4096, 2048, "G=256 V=2 B=4 WPE=4 cached"),
-    ("ATA_X", 0, 4096, 2048, "G=512 V=2 B=8 WPE=2 cached"),
+    ("MATVEC", 0, 4096, 2048, "G=256 V=2 B=4 WPE=4 nt"),
+    ("ATA_X", 0, 4096, 2048, "G=512 V=2 B=8 WPE=2 nt"),
     ("AXPBY_MV", 0, 2048, 4096, "G=256 V=4 B=1 WPE=4 nt"),
     ("MATVEC", 0, 1024, 16384, "G=512 V=8 B=2 WPE=2 nt cyclic cus=32/32"),
     ("BICG", 0, 1024, 16384, "G=512 V=8 B=2 WPE=2 cached"),
+    ("MATVEC", 0, 6553, 2560, "G=256 V=4 B=2 WPE=4 nt"),
+    ("MATVEC_T", 0, 5461, 3072, "G=512 V=2 B=8 WPE=2 nt"),
+    ("MATVEC_T", 0, 4096, 6144, "G=512 V=4 B=4 WPE=2 cached"),
+    ("ATA_X", 0, 2340, 7168, "G=512 V=4 B=4 WPE=2 cached"),
+    ("BICG", 0, 13107, 1280, "G=512 V=1 B=8 WPE=4 nt"),
+    ("MATVEC", 1, 2340, 3584, "G=512 V=4 B=4 WPE=2 nt"),
+    # 257-512-vector rows on 512-vector shapes
+    ("MATVEC", 0, 209715, 1280, "G=512 V=1 B=8 WPE=4 nt"),
+    ("ATA_X", 1, 209715, 640, "G=512 V=1 B=8 WPE=4 nt"),
+    ("AXPBY_MV", 0, 104857, 1280, "G=512 V=1 B=4 WPE=4 nt"),
+    # streamed rows that fill their group: the next wider shape
+    ("MATVEC", 0, 74898, 3584, "G=512 V=4 B=4 WPE=2 nt"),
+    ("BICG", 0, 74898, 3584, "G=512 V=2 B=8 WPE=2 nt"),
+    ("ATA_X", 1, 37449, 3584, "G=1024 V=4 B=2 WPE=4 nt"),
+    ("BICG", 0, 37449, 7168, "G=1024 V=2 B=4 WPE=4 nt"),
+    ("MATVEC_T", 0, 37449, 7168, "G=512 V=8 B=2 WPE=2 nt cyclic cus=32/32"),
+    ("MATVEC", 0, 43690, 6144, "G=512 V=8 B=2 WPE=2 nt"),
+    ("MATVEC_T", 0, 1 << 23, 320, "G=64 V=2 B=4 WPE=4 nt"),
+    ("ATA_X", 0, 1 << 21, 512, "G=64 V=4 B=2 WPE=4 nt"),
 ]
 
 
@@ -260,5 +279,13 @@ def test_harness_errors(L):
     assert L.mep_select_variant(ctypes.byref(c), 0, 30, 3, 1, 0, 1e-4, 0, ctypes.byref(best), None, 0) == mep.MEP_EINVAL
     assert "out-of-place" in mep.mep_last_error()
     c.A = c.out2 = None
+    # a flush buffer that is not a whole number of 16-byte vectors, or not
+    # 16-byte aligned, is refused before anything runs
+    c.op = mep.MEP_OP_ATA_X
+    c.flush_buf, c.flush_bytes = FAKE, 1000
+    assert L.mep_select_variant(ctypes.byref(c), 0, 30, 3, 1, 0, 1e-4, 0, ctypes.byref(best), None, 0) == mep.MEP_EALIGN
+    c.flush_buf, c.flush_bytes = FAKE + 8, 1024
+    assert L.mep_select_variant(ctypes.byref(c), 0, 30, 3, 1, 0, 1e-4, 0, ctypes.byref(best), None, 0) == mep.MEP_EALIGN
+    c.flush_buf, c.flush_bytes = None, 0
     c.op = 77
     assert L.mep_select_variant(ctypes.byref(c), 0, 30, 3, 1, 0, 1e-4, 0, ctypes.byref(best), None, 0) == mep.MEP_EINVAL

@@ -356,6 +356,14 @@ def test_select_variant_eqs_3_to_5(op, shape):
         call = mep.make_call(code, T["A"], in0=T["w"], out0=out0)
     else:
         call = mep.make_call(code, T["A"], in0=T["x"], B=T["B"], alpha=1.5, beta=1.2, out0=out0)
+    # warm timing (flush=False) with a flush buffer: the caches are cleared
+    # once before each candidate; a buffer of a size that is not a multiple
+    # of 16 bytes is refused before anything runs
+    fb = torch.empty(16 << 20, dtype=torch.uint8, device=dev)
+    call.flush_buf, call.flush_bytes = fb.data_ptr(), fb.numel() - 8
+    with pytest.raises(mep.MepError):
+        mep.mep_select_variant(call, warmup=1, R=7, k=2, tol=1e-4, apply=True)
+    call.flush_bytes = fb.numel()
     best, res = mep.mep_select_variant(call, warmup=1, R=7, k=2, tol=1e-4, apply=True)
     assert len(res) == mep.mep_variant_count(code, mep.MEP_F32, m, n)
     assert all(ok for _, _, ok in res), res
