@@ -167,22 +167,31 @@ static Cfg preferred_shape(int mode, int esize, int64_t m, int64_t n, int64_t nv
             return Cfg{1024, 4, 2, 4, 2};
         return Cfg{512, 8, 2, 2, 2};
     }
-    // Longer rows.  Streamed rows that fill their group more than 7/8: one
-    // matrix on 22 (ATAX) or 24 compute units per XCD for 4096-vector rows, 26
-    // for 8192-vector rows; two matrices (half the rows per batch,
-    // 4096-vector column panels) on 22 for 4096-vector rows and all 32
-    // beyond.  Emptier groups keep fewer bytes in flight and use every
-    // compute unit.  Cached: y = A x and GESUMMV still read non-temporally
-    // (~10% faster), the column-sum modes cached.
+    // Longer rows (4096- and 8192-vector shapes).  Streamed, one matrix:
+    // rows of 2049-4096 vectors on 24 compute units per XCD (ATAX rows past
+    // 7/8 of the group on 22; BICG only past 11/16), 8192-vector rows past
+    // 11/16 on 26, A^T w on 26
+    // then 24 (3-7% faster than all 32 wherever the row is longer than 2048
+    // vectors).  Two matrices (half the rows per batch, 4096-vector column
+    // panels beyond): streamed on 24 up to 4096 vectors, cache-resident on 24
+    // past them.  Cache-resident: the column-sum modes read cached; y = A x of
+    // rows short of 8192 vectors on 1024 x 8 x 1 at 4 waves per SIMD (4-9%).
+    // Rows cut into column panels (past 8192 vectors) use every compute unit.
     const int laux = stream || !col ? 2 : 0;
-    const bool full = (nv > 3584 && nv <= 4096) || (nv > 7168 && nv <= 8192);  // longer: column panels
-    if (nv <= 4096 || two) {
-        const int cux = !stream || !full ? kCusPerXcd
-                        : two ? (nv <= 4096 ? 22 : kCusPerXcd)
-                              : ((mode & F_FROMDOT) ? 22 : 24);
+    const bool panelled = nv > 8192;
+    if (two) {
+        const int cux = !panelled && (stream ? nv <= 4096 : nv > 4096) ? 24 : kCusPerXcd;
+        return Cfg{512, 8, 2, 2, 2, 0, cux};
+    }
+    if (nv <= 4096) {
+        const int cux = !stream || (bicg && nv <= 2816) ? kCusPerXcd : (atax && nv > 3584 ? 22 : 24);
         return Cfg{512, 8, 2, 2, laux, 0, cux};
     }
-    return Cfg{512, 16, 1, 2, laux, 0, stream && full ? 26 : kCusPerXcd};
+    if (!stream)
+        return mv && nv <= 7680 ? Cfg{1024, 8, 1, 4, 2} : Cfg{512, 16, 1, 2, laux};
+    const int64_t narrow_from = bicg && esize == 8 ? 6656 : 5632;  // fp64 BICG: past 13/16
+    const int cux = panelled ? kCusPerXcd : (atw ? (nv <= 5632 ? 26 : 24) : (nv > narrow_from ? 26 : kCusPerXcd));
+    return Cfg{512, 16, 1, 2, 2, 0, cux};
 }
 
 // The default of the element-wise path: the narrowest row group that holds

@@ -128,7 +128,7 @@ MEASURED_DEFAULTS = [
     ("BICG", 1, 131072, 1024, "G=512 V=1 B=8 WPE=4 nt"),
     ("MATVEC", 0, 32768, 8192, "G=512 V=8 B=1 WPE=4 nt"),
     ("BICG", 0, 32768, 8192, "G=512 V=8 B=2 WPE=2 nt cyclic cus=32/32"),
-    ("AXPBY_MV", 0, 8192, 16384, "G=512 V=8 B=1 WPE=2 nt cyclic cus=22/32"),
+    ("AXPBY_MV", 0, 8192, 16384, "G=512 V=8 B=1 WPE=2 nt cyclic cus=24/32"),
     ("GEMVER", 0, 131072, 2048, "G=512 V=2 B=8 WPE=2 nt"),
     ("GEMVER", 1, 131072, 1024, "G=256 V=4 B=2 WPE=4 nt"),
     # narrow rows: as many lanes per row as the row has vectors
@@ -140,7 +140,11 @@ MEASURED_DEFAULTS = [
     # rows between the measured lengths: the smallest 512-lane shape that covers them
     ("ATA_X", 0, 65472, 4100, "G=512 V=4 B=4 WPE=2 nt cyclic cus=32/32"),
     ("BICG", 0, 87267, 3076, "G=512 V=2 B=8 WPE=2 nt"),
-    ("ATA_X", 0, 21838, 12292, "G=512 V=8 B=2 WPE=2 nt cyclic cus=32/32"),
+    ("ATA_X", 0, 21838, 12292, "G=512 V=8 B=2 WPE=2 nt cyclic cus=24/32"),
+    ("MATVEC_T", 0, 13107, 20480, "G=512 V=16 B=1 WPE=2 nt cyclic cus=26/32"),
+    ("BICG", 0, 13107, 20480, "G=512 V=16 B=1 WPE=2 nt cyclic cus=32/32"),
+    ("ATA_X", 1, 10922, 12288, "G=512 V=16 B=1 WPE=2 nt cyclic cus=26/32"),
+    ("MATVEC", 0, 1024, 20480, "G=1024 V=8 B=1 WPE=4 nt"),
     # cache-resident
     ("MATVEC", 0, 4096, 2048, "G=256 V=2 B=4 WPE=4 nt"),
     ("ATA_X", 0, 4096, 2048, "G=512 V=2 B=8 WPE=2 nt"),
