@@ -119,8 +119,8 @@ static Cfg preferred_shape(int mode, int esize, int64_t m, int64_t n, int64_t nv
     // 257-512 vectors: 512-vector shapes (the 1024-vector ones left a row of
     // 320 vectors 15-30% slower): y = A x and GESUMMV of cache-resident
     // matrices on 256-lane groups, the rest on 512 lanes x 1 vector with
-    // 8-row batches.  Rows past 3/4 of the group (y = A x: 7/8) go to the
-    // 1024-vector shapes; cache-resident ATAX and fp32 BICG only past 7/8,
+    // 8-row batches.  Rows past 3/4 of the group go to the 1024-vector
+    // shapes; cache-resident ATAX and fp32 BICG only past 7/8,
     // fp64 BICG (the most registers per row) never, and streamed fp64 BICG
     // rows up to 3/4 run 2-12% faster on 256 x 2 x 4.
     if (nv <= 512) {
@@ -128,7 +128,7 @@ static Cfg preferred_shape(int mode, int esize, int64_t m, int64_t n, int64_t nv
             return stream && nv <= 384 ? Cfg{256, 2, 4, 4, 2} : Cfg{512, 1, 8, 4, 2};
         if (!stream && (mv || two))
             return Cfg{256, 2, 4, 4, 2};
-        if (nv <= 384 || (nv <= 448 && (mv || bicg || (atax && !stream))))
+        if (nv <= 384 || (nv <= 448 && (bicg || (atax && !stream))))
             return Cfg{512, 1, 8, 4, 2};
         if (atw || bicg || (atax && !stream) || (two && esize == 4))
             return Cfg{512, 2, 8, 2, 2};
@@ -136,36 +136,35 @@ static Cfg preferred_shape(int mode, int esize, int64_t m, int64_t n, int64_t nv
     }
     // 513-1024 vectors: 512 lanes x 2 vectors, 8-row batches; y = A x and
     // GESUMMV of cache-resident matrices on 256 x 4 (10-20% faster).
-    // Streamed rows that fill the group 7/8 or more run 3% faster on
-    // 512 x 4 x 4 (BICG: fp32 rows past 7/8 only).
+    // Streamed: A^T w, and the other modes for rows that fill the group 7/8
+    // or more, on 24 compute units per XCD (2-4% faster), except BICG (fp32
+    // rows past 7/8: 512 x 4 x 4), GESUMMV past 7/8 and y = A x from 7/8 to
+    // 15/16 (512 x 4 x 4).
     if (nv <= 1024) {
         if (!stream)
             return mv || two ? Cfg{256, 4, 2, 4, 2} : Cfg{512, 2, 8, 2, 2};
         if (bicg)
             return esize == 4 && nv > 896 ? Cfg{512, 4, 4, 2, 2} : Cfg{512, 2, 8, 2, 2};
-        return nv >= 896 ? Cfg{512, 4, 4, 2, 2} : Cfg{512, 2, 8, 2, 2};
+        if (nv >= 896 && (two || (mv && nv <= 960)))
+            return Cfg{512, 4, 4, 2, 2};
+        return atw || nv >= 896 ? Cfg{512, 2, 8, 2, 2, 0, 24} : Cfg{512, 2, 8, 2, 2};
     }
-    // 1025-2048 vectors: 512 lanes x 4 vectors, 4-row batches.  Streamed rows
-    // past ~13/16 of the group (y = A x: past ~11/16) run 2-6% faster on the
-    // 4096-vector shapes: 512 x 8 x 2, and for ATAX and BICG 1024-lane groups
-    // up to 15/16; y = A x of rows in the last 1/8 takes 1-row batches at 4
-    // waves per SIMD.  Cache-resident A^T w, and BICG and ATAX past ~13/16,
-    // read cached (the only place where cached loads are measurably faster).
+    // 1025-2048 vectors: 512 lanes x 4 vectors, 4-row batches; streamed on 24
+    // compute units per XCD (2-7% faster; BICG from 1408 vectors on; A^T w
+    // and GESUMMV of full rows on 512 x 8 x 2).  Cache-resident A^T w, and BICG and ATAX
+    // above 1664 vectors, read cached (the only place where cached loads are
+    // measurably faster).
     if (nv <= 2048) {
         if (!stream) {
             if (mv || two)
                 return Cfg{512, 4, 4, 2, 2};
             return Cfg{512, 4, 4, 2, atw || nv > 1664 ? 0 : 2};
         }
-        if (mv)
-            return nv <= 1408 ? Cfg{512, 4, 4, 2, 2} : (nv <= 1792 ? Cfg{512, 8, 2, 2, 2} : Cfg{512, 8, 1, 4, 2});
-        if (nv <= 1664)
+        if ((atw || two) && nv > 1920)
+            return Cfg{512, 8, 2, 2, 2};
+        if (bicg && nv <= 1408)
             return Cfg{512, 4, 4, 2, 2};
-        if (nv <= 1920 && bicg)
-            return Cfg{1024, 2, 4, 4, 2};
-        if (nv <= 1920 && atax)
-            return Cfg{1024, 4, 2, 4, 2};
-        return Cfg{512, 8, 2, 2, 2};
+        return Cfg{512, 4, 4, 2, 2, 0, 24};
     }
     // Longer rows (4096- and 8192-vector shapes).  Streamed, one matrix:
     // rows of 2049-4096 vectors on 24 compute units per XCD (ATAX rows past

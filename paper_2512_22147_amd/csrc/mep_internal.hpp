@@ -30,7 +30,7 @@ constexpr int kCusPerXcd = 32;
 // Vector path (16-byte loads), ordered by row capacity G * V; among equal
 // capacities the preferred shape comes first (measured on MI355X: streaming
 // the matrix with non-temporal loads is faster for every shape).
-constexpr int kNumVecCfg = 51;
+constexpr int kNumVecCfg = 53;
 constexpr Cfg kVecCfg[kNumVecCfg] = {
     // rows of 1-8 vectors: 2, 4 or 8 lanes per row, 32, 16 or 8 rows per wave
     {2, 1, 8, 4, 2},     {2, 1, 8, 4, 0},
@@ -44,9 +44,11 @@ constexpr Cfg kVecCfg[kNumVecCfg] = {
     {256, 2, 4, 4, 2},   {256, 2, 4, 4, 0},   {512, 1, 8, 4, 2},
     // 1024 vectors
     {256, 4, 2, 4, 2},   {256, 4, 2, 4, 0},   {512, 2, 8, 2, 2},   {512, 2, 8, 2, 0},
+    {512, 2, 8, 2, 2, 0, 24},
     {512, 2, 4, 4, 2},   {1024, 1, 8, 4, 2},
     // 2048 vectors
     {1024, 2, 4, 4, 2},  {1024, 2, 4, 4, 0},  {512, 4, 4, 2, 2},   {512, 4, 4, 2, 0},
+    {512, 4, 4, 2, 2, 0, 24},
     // 4096 vectors: a 16384-element fp32 row
     {512, 8, 2, 2, 2, 0, 24}, {512, 8, 2, 2, 2, 0, 22}, {512, 8, 2, 2, 2}, {512, 8, 2, 2, 2, 1},
     {1024, 4, 2, 4, 2},  {1024, 4, 2, 4, 2, 0, 24}, {512, 8, 1, 4, 2}, {256, 16, 1, 2, 2},

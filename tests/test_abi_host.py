@@ -122,12 +122,13 @@ MEASURED_DEFAULTS = [
     ("GEMVER", 0, 16384, 16384, "G=1024 V=4 B=2 WPE=4 nt cyclic cus=32/32"),
     ("MATVEC", 0, 16384, 16384, "G=512 V=8 B=2 WPE=2 nt cyclic cus=24/32"),
     # other row lengths, streamed
-    ("ATA_X", 0, 65536, 4096, "G=512 V=4 B=4 WPE=2 nt cyclic cus=32/32"),
+    ("ATA_X", 0, 65536, 4096, "G=512 V=2 B=8 WPE=2 nt cyclic cus=24/32"),
     ("MATVEC_T", 0, 131072, 2048, "G=512 V=2 B=8 WPE=2 nt"),
     ("MATVEC", 0, 131072, 2048, "G=512 V=2 B=4 WPE=4 nt"),
     ("BICG", 1, 131072, 1024, "G=512 V=1 B=8 WPE=4 nt"),
-    ("MATVEC", 0, 32768, 8192, "G=512 V=8 B=1 WPE=4 nt"),
-    ("BICG", 0, 32768, 8192, "G=512 V=8 B=2 WPE=2 nt cyclic cus=32/32"),
+    ("MATVEC", 0, 32768, 8192, "G=512 V=4 B=4 WPE=2 nt cyclic cus=24/32"),
+    ("BICG", 0, 32768, 8192, "G=512 V=4 B=4 WPE=2 nt cyclic cus=24/32"),
+    ("MATVEC_T", 0, 32768, 8192, "G=512 V=8 B=2 WPE=2 nt cyclic cus=32/32"),
     ("AXPBY_MV", 0, 8192, 16384, "G=512 V=8 B=1 WPE=2 nt cyclic cus=24/32"),
     ("GEMVER", 0, 131072, 2048, "G=512 V=2 B=8 WPE=2 nt"),
     ("GEMVER", 1, 131072, 1024, "G=256 V=4 B=2 WPE=4 nt"),
@@ -138,7 +139,7 @@ MEASURED_DEFAULTS = [
     ("BICG", 0, 1 << 25, 8, "G=2 V=1 B=8 WPE=4 nt"),
     ("BICG", 1, 1 << 22, 32, "G=16 V=1 B=4 WPE=4 nt"),
     # rows between the measured lengths: the smallest 512-lane shape that covers them
-    ("ATA_X", 0, 65472, 4100, "G=512 V=4 B=4 WPE=2 nt cyclic cus=32/32"),
+    ("ATA_X", 0, 65472, 4100, "G=512 V=4 B=4 WPE=2 nt cyclic cus=24/32"),
     ("BICG", 0, 87267, 3076, "G=512 V=2 B=8 WPE=2 nt"),
     ("ATA_X", 0, 21838, 12292, "G=512 V=8 B=2 WPE=2 nt cyclic cus=24/32"),
     ("MATVEC_T", 0, 13107, 20480, "G=512 V=16 B=1 WPE=2 nt cyclic cus=26/32"),
@@ -162,12 +163,14 @@ MEASURED_DEFAULTS = [
     ("ATA_X", 1, 209715, 640, "G=512 V=1 B=8 WPE=4 nt"),
     ("AXPBY_MV", 0, 104857, 1280, "G=512 V=1 B=4 WPE=4 nt"),
     # streamed rows that fill their group: the next wider shape
-    ("MATVEC", 0, 74898, 3584, "G=512 V=4 B=4 WPE=2 nt"),
+    ("MATVEC", 0, 74898, 3584, "G=512 V=4 B=4 WPE=2 nt cyclic cus=32/32"),
+    ("MATVEC", 0, 65536, 4096, "G=512 V=2 B=8 WPE=2 nt cyclic cus=24/32"),
     ("BICG", 0, 74898, 3584, "G=512 V=2 B=8 WPE=2 nt"),
-    ("ATA_X", 1, 37449, 3584, "G=1024 V=4 B=2 WPE=4 nt"),
-    ("BICG", 0, 37449, 7168, "G=1024 V=2 B=4 WPE=4 nt"),
-    ("MATVEC_T", 0, 37449, 7168, "G=512 V=8 B=2 WPE=2 nt cyclic cus=32/32"),
-    ("MATVEC", 0, 43690, 6144, "G=512 V=8 B=2 WPE=2 nt"),
+    ("ATA_X", 1, 37449, 3584, "G=512 V=4 B=4 WPE=2 nt cyclic cus=24/32"),
+    ("BICG", 0, 37449, 7168, "G=512 V=4 B=4 WPE=2 nt cyclic cus=24/32"),
+    ("BICG", 0, 52428, 5120, "G=512 V=4 B=4 WPE=2 nt cyclic cus=32/32"),
+    ("MATVEC_T", 0, 37449, 7168, "G=512 V=4 B=4 WPE=2 nt cyclic cus=24/32"),
+    ("MATVEC", 0, 43690, 6144, "G=512 V=4 B=4 WPE=2 nt cyclic cus=24/32"),
     ("MATVEC_T", 0, 1 << 23, 320, "G=64 V=2 B=4 WPE=4 nt"),
     ("ATA_X", 0, 1 << 21, 512, "G=64 V=4 B=2 WPE=4 nt"),
 ]
