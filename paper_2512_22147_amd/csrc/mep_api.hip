@@ -195,10 +195,20 @@ static Cfg preferred_shape(int mode, int esize, int64_t m, int64_t n, int64_t nv
 
 // The default of the element-wise path: the narrowest row group that holds
 // the row, with 16 elements per lane in flight for fp32 and 8 for fp64 (64
-// bytes either way; deeper fp64 batches spill).
-static Cfg preferred_scalar_shape(int esize, int64_t n)
+// bytes either way).  Measured exceptions (cleared caches before each
+// candidate): fp64 rows longer than 128 elements of a streamed matrix, and
+// fp64 BICG rows longer than 1024, take 16 (4-22% faster); fp32 rows that
+// fill more than 7/8 of a 256- or 1024-lane group take 8, except BICG (2-9%).
+static Cfg preferred_scalar_shape(int mode, int esize, int64_t m, int64_t n)
 {
-    const int per_lane = esize == 4 ? 16 : 8;
+    const bool bicg = mode == MODE_BICG;
+    const bool stream = ((mode & F_TWO) ? 2 : 1) * m * n * esize > (int64_t(128) << 20);
+    int per_lane = esize == 4 ? 16 : 8;
+    if (esize == 8 && ((stream && n > 128) || (bicg && n > 1024)))
+        per_lane = 16;
+    const int64_t cap = n <= 512 ? 512 : (n <= 1024 ? 1024 : 8192);  // G x V of the shapes below
+    if (esize == 4 && !bicg && n > 256 && n <= 8192 && 8 * n > 7 * cap)
+        per_lane = 8;
     if (n <= 64) {
         const int g = n <= 8 ? 8 : (n <= 16 ? 16 : (n <= 32 ? 32 : 64));
         return Cfg{g, 1, per_lane, 4, 2};
@@ -254,7 +264,7 @@ int stream_candidates(int esize, bool vec, int mode, int64_t m, int64_t n, int* 
     }
     // the measured default goes first when it is among the candidates
     {
-        const Cfg want = vec ? preferred_shape(mode, esize, m, n, nv) : preferred_scalar_shape(esize, n);
+        const Cfg want = vec ? preferred_shape(mode, esize, m, n, nv) : preferred_scalar_shape(mode, esize, m, n);
         for (int k = 1; k < cnt; ++k) {
             if (same_cfg(tab[idx[k]], want)) {
                 const int keep = idx[k];
