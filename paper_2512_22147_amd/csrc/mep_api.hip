@@ -262,17 +262,30 @@ int stream_candidates(int esize, bool vec, int mode, int64_t m, int64_t n, int* 
                 (int64_t)tab[i].G * tab[i].V == best)
                 idx[cnt++] = i;
     }
-    // the measured default goes first when it is among the candidates
+    // the measured default goes first; when the capacity window above left it
+    // out (or the list was full), it is taken from the whole table, as long
+    // as it fits this mode's register and LDS budget
     {
         const Cfg want = vec ? preferred_shape(mode, esize, m, n, nv) : preferred_scalar_shape(mode, esize, m, n);
-        for (int k = 1; k < cnt; ++k) {
-            if (same_cfg(tab[idx[k]], want)) {
-                const int keep = idx[k];
-                for (int j = k; j > 0; --j)
-                    idx[j] = idx[j - 1];
-                idx[0] = keep;
-                break;
+        int at = -1;
+        for (int k = 0; k < cnt && at < 0; ++k)
+            if (same_cfg(tab[idx[k]], want))
+                at = k;
+        if (at < 0) {
+            for (int i = 0; i < nt && at < 0; ++i) {
+                if (same_cfg(tab[i], want) && cfg_fits(tab[i], mode, vgpr32) && (int64_t)tab[i].G * tab[i].V >= std::min<int64_t>(nv, 8192)) {
+                    if (cnt < 16)
+                        ++cnt;
+                    at = cnt - 1;
+                    idx[at] = i;
+                }
             }
+        }
+        if (at > 0) {
+            const int keep = idx[at];
+            for (int j = at; j > 0; --j)
+                idx[j] = idx[j - 1];
+            idx[0] = keep;
         }
     }
     return cnt;
