@@ -20,8 +20,10 @@ from tests.gpu_cases import TOL, normwise
 pytestmark = pytest.mark.gpu
 
 # (dtype, m, n): 65600 x 32768 fp32 = 2,149,580,800 elements (8.6 GB per
-# matrix, two for GESUMMV); 33000 x 16384 fp64 = 4.3 GB per matrix
-CASES = [("f32", 65600, 32768), ("f64", 33000, 16384)]
+# matrix, two for GESUMMV); 33000 x 16384 fp64 = 4.3 GB per matrix; and
+# 33000 x 16383 fp64, whose rows are not 16-byte aligned (the element-wise
+# path, over two column panels)
+CASES = [("f32", 65600, 32768), ("f64", 33000, 16384), ("f64", 33000, 16383)]
 
 
 @pytest.fixture(autouse=True)
