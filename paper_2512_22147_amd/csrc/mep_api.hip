@@ -102,18 +102,28 @@ static Cfg preferred_shape(int mode, int esize, int64_t m, int64_t n, int64_t nv
     }
     if (nv <= 256)
         return Cfg{64, 4, 2, 4, naux};
-    // the rank-2 update that stores Ahat (GEMVER's first pass): 512-lane groups
-    // sized to the row up to 2048 vectors (fp64 rows of <= 512 vectors on
-    // 256 x 4, where 512 x 2 x 8 spills), 1024-lane groups with 4 vectors per
-    // lane beyond (panels past 4096 vectors)
+    // the rank-2 update that stores Ahat (GEMVER's first pass), from sweeps
+    // with cleared caches: streamed rows of up to 7/8 of 1024 vectors on
+    // 256 x 4 x 2 (fp32 rows of 449-512 vectors on 512 x 2 x 8), fuller ones
+    // on 512 x 4 x 4 (fp64: 512 x 2 x 8), 1025-2048 vectors on 512 x 4 x 4,
+    // 1024 x 4 x 2 beyond; cache-resident (cached loads) 256 x 4 x 2 up to 352
+    // vectors, 512 x 2 x 8 up to 1024, then as streamed
     if (mode & F_STORE) {
         const int aux = stream ? 2 : 0;
-        if (nv <= 512)
-            return stream && esize == 8 ? Cfg{256, 4, 2, 4, 2} : Cfg{512, 2, 8, 2, aux};
-        if (nv <= 1024)
-            return stream ? Cfg{512, 4, 4, 2, 2} : Cfg{512, 2, 8, 2, 0};
+        if (nv <= 512) {
+            if (stream)
+                return esize == 8 || nv <= 448 ? Cfg{256, 4, 2, 4, 2} : Cfg{512, 2, 8, 2, 2};
+            return nv <= 352 ? Cfg{256, 4, 2, 4, 0} : Cfg{512, 2, 8, 2, 0};
+        }
+        if (nv <= 1024) {
+            if (!stream)
+                return Cfg{512, 2, 8, 2, 0};
+            if (nv < 896)
+                return Cfg{256, 4, 2, 4, 2};
+            return esize == 8 ? Cfg{512, 2, 8, 2, 2} : Cfg{512, 4, 4, 2, 2};
+        }
         if (nv <= 2048)
-            return stream ? Cfg{512, 8, 2, 2, 2} : Cfg{512, 4, 4, 2, 0};
+            return Cfg{512, 4, 4, 2, aux};
         return Cfg{1024, 4, 2, 4, aux};
     }
     // 257-512 vectors: 512-vector shapes (the 1024-vector ones left a row of
