@@ -92,9 +92,10 @@ static Cfg preferred_shape(int mode, int esize, int64_t m, int64_t n, int64_t nv
         return bicg ? Cfg{16, 1, 4, 4, 2} : Cfg{16, 1, 8, 4, naux, 0, 16};
     if (nv <= 64)
         return Cfg{64, 1, 8, 4, naux};
-    // 65-128 vectors: 2 vectors per lane; A^T w and ATAX of streamed rows that
-    // fill them take 4 (half the rows per batch; 13-15% slower for 80-vector
-    // rows, a few % faster for 128), and so does GEMVER's first pass
+    // 65-128 vectors: 2 vectors per lane.  A^T w and ATAX of streamed rows
+    // that fill more than 7/8 of them take 4 with half the rows per batch (a
+    // few % faster there; the same shape is 13-15% slower for 80-vector
+    // rows), and so does GEMVER's first pass
     if (nv <= 128) {
         if ((mode & F_STORE) || ((atw || atax) && stream && nv > 112))
             return Cfg{64, 4, 2, 4, naux};
