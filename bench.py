@@ -39,6 +39,10 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HEADLINE = "ata_x_16384"
+# the other benchmark configurations (parity cases), timed beside the headline:
+# whole steps (all kernels of the operation) on resident inputs, the default shape
+OTHER_CONFIGS = [("ata_x_1024", "f32"), ("bicg_4096", "f32"), ("axpby_mv_8192", "f32"),
+                 ("matvec_t_1m_x_64", "f32")]
 HEADLINE_METRIC = "achieved HBM GB/s (and % of MI355X peak) for y=Aᵀ(Ax), fp32 16384²"
 PEAK_GBS = 8000.0
 KERNEL_SOURCE = "paper_2512_22147_amd/csrc/mep_kernels.hpp"
@@ -92,6 +96,9 @@ def parse():
                          "the chosen shape's standalone speedup over the default (Sec. 4.1.3)")
     ap.add_argument("--no-eq3", action="store_true",
                     help="skip the Eq. 3 cold-cache timing (R = 30, k = 3, 1 GiB flush per sample)")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the step timing of the other benchmark configurations (reported beside "
+                         "the headline as other_configs)")
     return ap.parse_args()
 
 
@@ -504,6 +511,17 @@ def main():
             "traffic": measured_traffic(args.workload, "f64", sec["config"]),
             "kernel_config": sec["config"], "eq3": sec["eq3"],
         }
+    others = None
+    if args.workload == HEADLINE and not args.no_configs:
+        others = []
+        for wl, dt in OTHER_CONFIGS:
+            r = run_gpu(wl, dt, args.steps, args.warmup, -1, False)
+            others.append({
+                "workload": wl, "dtype": dt, "m": r["m"], "n": r["n"],
+                "ms_per_step": round(r["ms_per_step"], 5), "value": round(r["value_gbs"], 1), "unit": "GB/s",
+                "kernel_gbs": round(r["kernel_gbs"], 1), "kernel_frac": round(r["kernel_gbs"] / PEAK_GBS, 4),
+                "kernel_config": r["config"],
+            })
     copy = probe_copy() if args.probe_copy else None
     selection = select_round(args.workload, args.dtype) if args.select else None
     w = prim["w"]
@@ -542,6 +560,7 @@ def main():
         "cpu_baseline": cpu,
         "fe_error_vs_oracle": fe,
         "secondary": secondary,
+        "other_configs": others,
         "copy_probe": copy,
         "hbm_ceiling_probe": ceiling,
         "mep_budget": mep_budget(w, args.dtype, prim["kernel_ms"], t_mep),
