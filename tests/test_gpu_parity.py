@@ -443,6 +443,28 @@ def _random_cases(count=72, seed=2026):
 RANDOM_CASES = _random_cases()
 
 
+def _random_streamed_cases(count=24, seed=99):
+    """Seeded random shapes of matrices too large for the Infinity Cache
+    (150-400 MB), where the default shapes differ from the cache-resident
+    ones (narrowed grids, other batch depths): row lengths of 1 to ~40000
+    elements, every op and both dtypes."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    while len(cases) < count:
+        n = int(np.exp(rng.uniform(0, np.log(40000))))
+        dt = DTYPES[int(rng.integers(2))]
+        es = np.dtype(dt).itemsize
+        m = max(1, int(rng.uniform(150e6, 400e6) / (n * es)))
+        op = OPS[int(rng.integers(len(OPS)))]
+        if op == "gemver" and m * n * es > 250e6:
+            continue
+        cases.append((op, m, n, dt))
+    return cases
+
+
+RANDOM_STREAMED_CASES = _random_streamed_cases()
+
+
 @pytest.mark.parametrize("case", range(len(RANDOM_CASES)))
 def test_random_shapes(case):
     op, m, n, dt = RANDOM_CASES[case]
@@ -450,3 +472,12 @@ def test_random_shapes(case):
     ref = oracle_outputs(op, ins, dt)
     got = gpu_outputs(op, ins, dt)
     assert_parity(op, got, ref, dt, what=f"case {case}: {op} {m}x{n} {np.dtype(dt).name}")
+
+
+@pytest.mark.parametrize("case", range(len(RANDOM_STREAMED_CASES)))
+def test_random_streamed_shapes(case):
+    op, m, n, dt = RANDOM_STREAMED_CASES[case]
+    ins = make_inputs(op, m, n, dt, seed=9100 + case)
+    ref = oracle_outputs(op, ins, dt)
+    got = gpu_outputs(op, ins, dt)
+    assert_parity(op, got, ref, dt, what=f"streamed case {case}: {op} {m}x{n} {np.dtype(dt).name}")
