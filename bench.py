@@ -368,33 +368,40 @@ def cpu_model() -> str:
     return "unknown"
 
 
-def probe_ceiling():
-    """HBM read ceiling: the library's sum over ~2 GiB of fp32 (a pure stream;
-    the longest vector the library accepts, 65535 x 8192 elements)."""
+def probe_read(n: int, dtype: str = "f32", reps: int = 20) -> float:
+    """GB/s of the library's sum over n elements (a pure read of n * es
+    bytes), launched back to back, so an array that fits the 256 MB Infinity
+    Cache is read from there as a cache-resident matrix of the same size is."""
     import torch
 
     from paper_2512_22147_amd import mep
 
     dev = torch.device("cuda:0")
-    n = 65535 * 8192
-    x = torch.ones(n, dtype=torch.float32, device=dev)
-    s = torch.empty(1, dtype=torch.float32, device=dev)
-    ws = torch.empty(max(mep.mep_workspace_bytes(mep.MEP_OP_REDUCE_SUM, mep.MEP_F32, 1, n), 1),
+    tdt, code, es = (torch.float32, mep.MEP_F32, 4) if dtype == "f32" else (torch.float64, mep.MEP_F64, 8)
+    x = torch.ones(n, dtype=tdt, device=dev)
+    s = torch.empty(1, dtype=tdt, device=dev)
+    ws = torch.empty(max(mep.mep_workspace_bytes(mep.MEP_OP_REDUCE_SUM, code, 1, n), 1),
                      dtype=torch.uint8, device=dev)
     call = mep.make_call(mep.MEP_OP_REDUCE_SUM, x, out0=s, ws=ws)
     for _ in range(3):
         mep.mep_run(call)
     torch.cuda.synchronize()
-    reps = 20
     mep.mep_profile_begin(reps)
     for _ in range(reps):
         mep.mep_run(call)
     torch.cuda.synchronize()
     tot, cnt = mep.mep_profile_end()
-    gbs = n * 4 / (tot / cnt * 1e-3) / 1e9
-    log(f"[bench] HBM ceiling probe: sum of {n * 4} B fp32, {gbs:.1f} GB/s")
     del x, ws
     torch.cuda.empty_cache()
+    return n * es / (tot / cnt * 1e-3) / 1e9
+
+
+def probe_ceiling():
+    """HBM read ceiling: the library's sum over ~2 GiB of fp32 (a pure stream;
+    the longest vector the library accepts, 65535 x 8192 elements)."""
+    n = 65535 * 8192
+    gbs = probe_read(n)
+    log(f"[bench] HBM ceiling probe: sum of {n * 4} B fp32, {gbs:.1f} GB/s")
     return {"kernel": "k_reduce_sum (fp32, 65535 x 8192 elements)", "bytes_read": n * 4, "gbs": round(gbs, 1),
             "frac_of_peak": round(gbs / PEAK_GBS, 4)}
 
@@ -516,11 +523,16 @@ def main():
         others = []
         for wl, dt in OTHER_CONFIGS:
             r = run_gpu(wl, dt, args.steps, args.warmup, -1, False)
+            # a plain read of as many matrix bytes, from wherever they live
+            # (HBM, or the Infinity Cache for matrices of at most 128 MiB)
+            mats = 2 if r["w"].op == "axpby_mv" else 1
+            read_gbs = probe_read(mats * r["m"] * r["n"], dt)
             others.append({
                 "workload": wl, "dtype": dt, "m": r["m"], "n": r["n"],
                 "ms_per_step": round(r["ms_per_step"], 5), "value": round(r["value_gbs"], 1), "unit": "GB/s",
                 "kernel_gbs": round(r["kernel_gbs"], 1), "kernel_frac": round(r["kernel_gbs"] / PEAK_GBS, 4),
-                "kernel_config": r["config"],
+                "kernel_config": r["config"], "same_size_read_gbs": round(read_gbs, 1),
+                "kernel_frac_of_read": round(r["kernel_gbs"] / read_gbs, 4),
             })
     copy = probe_copy() if args.probe_copy else None
     selection = select_round(args.workload, args.dtype) if args.select else None
