@@ -51,7 +51,7 @@ constexpr int64_t kMaxRow = int64_t(65535) * 8192;
 static int esize_of(int dtype) { return dtype == MEP_F32 ? 4 : (dtype == MEP_F64 ? 8 : 0); }
 
 // The default shape for a row of nv vectors, from candidate sweeps on MI355X
-// (every operation, both element types, two boxes, rows of 1-8192 vectors,
+// (every operation, both element types, two machines, rows of 1-8192 vectors,
 // matrices of 64 MiB that stay in the 256 MB Infinity Cache across calls and
 // of 1 GiB that stream from HBM).  What decides the shape is how much of each
 // row group holds data and how many bytes every compute unit keeps in
