@@ -14,8 +14,9 @@
  * ---------------------------------------
  * - Matrices are row-major and contiguous: element (i, j) of the m x n
  *   matrix A is A[i * n + j].  Vectors are contiguous.
- * - dtype is MEP_F32 or MEP_F64.  Every vector has that element type and the
- *   arithmetic is done in it (fp32 inputs accumulate in fp32).
+ * - dtype is MEP_F32 or MEP_F64 (a mep_dtype_t value, passed as an int).
+ *   Every vector has that element type and the arithmetic is done in it
+ *   (fp32 inputs accumulate in fp32).
  * - Device pointers are plain HIP device addresses (e.g. a torch tensor's
  *   data_ptr()).  Each must be aligned to its element size.  16-byte aligned
  *   matrices whose row length is a multiple of 16 bytes take the 16-byte
@@ -76,7 +77,12 @@ enum {
 
 typedef void* mep_stream_t; /* hipStream_t */
 
-/* Workspace bytes that op needs for an m x n problem of the given dtype. */
+/*
+ * Workspace bytes that op needs for an m x n problem of the given dtype
+ * (covers every kernel candidate and both load paths; 0 for bad arguments).
+ * No passage of the paper defines this call: it sizes the caller-owned
+ * scratch that the MEP statement's "allocate" step provides.
+ */
 size_t mep_workspace_bytes(int op, int dtype, int64_t m, int64_t n);
 
 /*
@@ -212,7 +218,8 @@ double mep_trimmed_mean(const double* samples, int R, int k);
  * host copy `out` (len elements of dtype) with a host fp64 reference.
  * *err = max_i |out_i - ref_i| / max_i |ref_i| (normwise relative error);
  * +inf if any out_i is not finite, or if ref is all zero and out is not.
- * *pass = (*err <= tol).  len = 0 passes with *err = 0.
+ * *pass = (*err <= tol).  len = 0 passes with *err = 0.  Every ref_i must be
+ * finite (MEP_EINVAL otherwise: a NaN reference would compare as agreeing).
  */
 int mep_check_fe(int dtype, const void* out, const double* ref, int64_t len, double tol,
                  double* err, int* pass);
@@ -227,6 +234,11 @@ int mep_check_fe(int dtype, const void* out, const double* ref, int64_t len, dou
  * 0; a v beyond the count of a later shape also means the default).
  * mep_workspace_bytes() already covers every candidate.  The setting is
  * process-wide; it changes speed only, never the checks or the contract.
+ * The count and the descriptions assume 16-byte aligned operands (the vector
+ * path) whenever the row length allows it; a call with unaligned operands
+ * takes the element-wise path, whose list differs.  An index is kept per op
+ * only: it means the candidate it named for the shape, dtype and load path
+ * it was chosen on, and some other candidate (or the default) elsewhere.
  */
 int mep_variant_count(int op, int dtype, int64_t m, int64_t n);
 int mep_set_variant(int op, int variant);
@@ -241,9 +253,13 @@ int mep_variant_info(int op, int dtype, int64_t m, int64_t n, int variant, char*
  * kernels for call->op at call's shape: candidate 0 (the default) is the
  * baseline K^(d); every candidate n runs once and its outputs are compared
  * with the baseline's by the FE metric of mep_check_fe (Eq. 4, tolerance
- * tol); each candidate that passes is timed with mep_time_trimmed(warmup, R,
- * k, inner, flush) (Eq. 3); *best receives the argmin of the trimmed means
- * over the passing candidates, the lower index on ties (Eq. 5).  With
+ * tol; every output of the call is judged on its own scale, GEMVER's Ahat
+ * included, and a non-finite output fails, the baseline's too); each
+ * candidate that passes is timed with mep_time_trimmed(warmup, R, k, inner,
+ * flush) (Eq. 3); *best receives the argmin of the trimmed means over the
+ * passing candidates, the lower index on ties (Eq. 5), or -1 when none
+ * passes.  The candidates are those of the load path the call really takes
+ * (its operands' alignment decides it, as for any call).  With
  * apply != 0 the winner becomes the op's variant (mep_set_variant), else the
  * previous setting is restored.  results (nullable, results_cap entries)
  * receives, per candidate, the trimmed mean (ms; NaN when not timed), the FE
@@ -252,10 +268,12 @@ int mep_variant_info(int op, int dtype, int64_t m, int64_t n, int variant, char*
  * call, the caches are cleared once (by writing the buffer) before each
  * candidate runs, so that no candidate's warm timing inherits the cache
  * state another one left behind.  A GEMVER call must be out of place (out2 !=
- * A), else MEP_EINVAL: each in-place run changes A.  The candidate set is fixed,
- * so one round is the whole search (the paper's D rounds regenerate
- * candidates; here nothing new appears in a later round).  Synchronizes
- * call->stream; overwrites the call's outputs.
+ * A), else MEP_EINVAL: each in-place run changes A.  Stop rule: the paper
+ * iterates until round D or until the gain falls below a threshold (Sec. 3.2,
+ * after Eq. 5), each round generating new candidates.  Here the candidate set
+ * is fixed, so a second round would only re-find the same argmin: one round
+ * is the whole search, and the call takes neither D nor a threshold.
+ * Synchronizes call->stream; overwrites the call's outputs.
  */
 typedef struct {
     double mean_ms;
@@ -268,6 +286,9 @@ int mep_select_variant(const mep_call_t* call, int warmup, int R, int k, int inn
                        int results_cap);
 
 /*
+ * No passage of the paper defines the calls from here to the end of the
+ * file: they are the library's own measurement and diagnostics.
+ *
  * Device-time instrumentation of each operation's dominant kernel (the
  * matrix-streaming kernel; the first stage of the sum; the vector add).
  * mep_profile_begin(cap) arms up to cap records; while armed, every operation

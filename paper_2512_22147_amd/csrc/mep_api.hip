@@ -1215,24 +1215,31 @@ int mep_time_trimmed(const mep_call_t* call, int warmup, int R, int k, int inner
     return MEP_OK;
 }
 
-// Lengths of a call's two outputs (out0, out1).
-static void output_lengths(const mep_call_t* c, int64_t* l0, int64_t* l1)
+// The outputs of a call (out0, out1, out2) and their lengths in elements.
+struct CallOutputs {
+    void* ptr[3];
+    int64_t len[3];
+};
+
+static CallOutputs call_outputs(const mep_call_t* c)
 {
-    *l1 = 0;
+    CallOutputs o{{c->out0, c->out1, c->out2}, {0, 0, 0}};
     switch (c->op) {
-    case MEP_OP_MATVEC: *l0 = c->m; break;
-    case MEP_OP_MATVEC_T: *l0 = c->n; break;
-    case MEP_OP_BICG: *l0 = c->n; *l1 = c->out1 ? c->m : 0; break;
-    case MEP_OP_ATA_X: *l0 = c->n; *l1 = c->out1 ? c->m : 0; break;
-    case MEP_OP_AXPBY_MV: *l0 = c->m; break;
-    case MEP_OP_REDUCE_SUM: *l0 = 1; break;
-    case MEP_OP_VECTOR_ADD: *l0 = c->n; break;
-    case MEP_OP_GEMVER: *l0 = c->n; *l1 = c->m; break;
-    default: *l0 = 0; break;
+    case MEP_OP_MATVEC: o.len[0] = c->m; break;
+    case MEP_OP_MATVEC_T: o.len[0] = c->n; break;
+    case MEP_OP_BICG: o.len[0] = c->n; o.len[1] = c->out1 ? c->m : 0; break;
+    case MEP_OP_ATA_X: o.len[0] = c->n; o.len[1] = c->out1 ? c->m : 0; break;
+    case MEP_OP_AXPBY_MV: o.len[0] = c->m; break;
+    case MEP_OP_REDUCE_SUM: o.len[0] = 1; break;
+    case MEP_OP_VECTOR_ADD: o.len[0] = c->n; break;
+    case MEP_OP_GEMVER: o.len[0] = c->n; o.len[1] = c->m; o.len[2] = c->m * c->n; break;
+    default: break;
     }
+    return o;
 }
 
-// Runs the call once and returns its outputs on the host, promoted to fp64.
+// Runs the call once and returns its outputs on the host, promoted to fp64,
+// one after another in the order out0, out1, out2.
 static int run_and_fetch(const mep_call_t* c, std::vector<double>& out)
 {
     int rc = mep_run(c);
@@ -1241,28 +1248,32 @@ static int run_and_fetch(const mep_call_t* c, std::vector<double>& out)
     hipError_t e = hipStreamSynchronize((hipStream_t)c->stream);
     if (e != hipSuccess)
         return hip_fail(e, "synchronize");
-    int64_t l0, l1;
-    output_lengths(c, &l0, &l1);
+    const CallOutputs o = call_outputs(c);
     const int es = esize_of(c->dtype);
-    std::vector<char> raw((size_t)(l0 + l1) * es + 1);
-    if (l0 > 0)
-        e = hipMemcpy(raw.data(), c->out0, (size_t)l0 * es, hipMemcpyDeviceToHost);
-    if (e == hipSuccess && l1 > 0)
-        e = hipMemcpy(raw.data() + (size_t)l0 * es, c->out1, (size_t)l1 * es, hipMemcpyDeviceToHost);
+    const int64_t total = o.len[0] + o.len[1] + o.len[2];
+    std::vector<char> raw((size_t)total * es + 1);
+    size_t at = 0;
+    for (int k = 0; k < 3 && e == hipSuccess; ++k) {
+        if (o.len[k] > 0)
+            e = hipMemcpy(raw.data() + at, o.ptr[k], (size_t)o.len[k] * es, hipMemcpyDeviceToHost);
+        at += (size_t)o.len[k] * es;
+    }
     if (e != hipSuccess)
         return hip_fail(e, "copy outputs");
-    out.resize((size_t)(l0 + l1));
-    for (int64_t i = 0; i < l0 + l1; ++i)
+    out.resize((size_t)total);
+    for (int64_t i = 0; i < total; ++i)
         out[i] = es == 4 ? (double)((const float*)raw.data())[i] : ((const double*)raw.data())[i];
     return MEP_OK;
 }
 
-// The FE metric of mep_check_fe on elements [lo, hi) of two host fp64 vectors.
+// The FE metric of mep_check_fe on elements [lo, hi) of two host fp64
+// vectors: +inf when either side holds a non-finite value (std::max would
+// skip a NaN reference entry and let an all-NaN reference pass).
 static double fe_metric(const std::vector<double>& out, const std::vector<double>& ref, size_t lo, size_t hi)
 {
     double worst = 0.0, scale = 0.0;
     for (size_t i = lo; i < hi; ++i) {
-        if (!std::isfinite(out[i]))
+        if (!std::isfinite(out[i]) || !std::isfinite(ref[i]))
             return std::numeric_limits<double>::infinity();
         scale = std::max(scale, std::fabs(ref[i]));
         worst = std::max(worst, std::fabs(out[i] - ref[i]));
@@ -1272,12 +1283,48 @@ static double fe_metric(const std::vector<double>& out, const std::vector<double
     return worst / scale;
 }
 
-// Each output of a call is judged on its own scale; the worse one counts.
+// Each output of a call is judged on its own scale; the worst one counts.
 static double fe_metric_call(const mep_call_t* c, const std::vector<double>& out, const std::vector<double>& ref)
 {
-    int64_t l0, l1;
-    output_lengths(c, &l0, &l1);
-    return std::max(fe_metric(out, ref, 0, (size_t)l0), fe_metric(out, ref, (size_t)l0, (size_t)(l0 + l1)));
+    const CallOutputs o = call_outputs(c);
+    double worst = 0.0;
+    size_t lo = 0;
+    for (int k = 0; k < 3; ++k) {
+        worst = std::max(worst, fe_metric(out, ref, lo, lo + (size_t)o.len[k]));
+        lo += (size_t)o.len[k];
+    }
+    return worst;
+}
+
+// The load path a call really takes (the 16-byte vector path needs the row
+// length and the streamed operands' addresses aligned, as each run_* checks),
+// and so the candidate list its variant index refers to.
+static bool call_vec(const mep_call_t* c)
+{
+    const int es = esize_of(c->dtype);
+    if (es == 0 || !vec_ok_n(es, c->n) || !aligned(c->A, 16))
+        return false;
+    switch (c->op) {
+    case MEP_OP_MATVEC:
+    case MEP_OP_ATA_X: return aligned(c->in0, 16);
+    case MEP_OP_BICG: return aligned(c->in1, 16);
+    case MEP_OP_AXPBY_MV: return aligned(c->B, 16) && aligned(c->in0, 16);
+    case MEP_OP_GEMVER: return aligned(c->out2, 16) && aligned(c->in1, 16) && aligned(c->in3, 16);
+    default: return true;
+    }
+}
+
+static int call_variant_count(const mep_call_t* c)
+{
+    if (is_vector_op(c->op))
+        return mep_variant_count(c->op, c->dtype, c->m, c->n);
+    const int es = esize_of(c->dtype);
+    const int mode = op_mode(c->op);
+    if (es == 0 || mode < 0 || c->m < 0 || c->n < 0 || c->m > kMaxDim || c->n > kMaxDim)
+        return 0;
+    int idx[16];
+    return std::max(1, stream_candidates(es, call_vec(c), mode, std::max<int64_t>(c->m, 1),
+                                         std::max<int64_t>(c->n, 1), idx));
 }
 
 int mep_select_variant(const mep_call_t* call, int warmup, int R, int k, int inner, int flush, double tol,
@@ -1294,7 +1341,7 @@ int mep_select_variant(const mep_call_t* call, int warmup, int R, int k, int inn
     const bool have_flush = call->flush_buf != nullptr && call->flush_bytes > 0;
     if (have_flush && (!aligned(call->flush_buf, 16) || call->flush_bytes % 16))
         return fail(MEP_EALIGN, "flush buffer must be 16-byte aligned and a multiple of 16 bytes");
-    const int count = mep_variant_count(call->op, call->dtype, call->m, call->n);
+    const int count = call_variant_count(call);
     if (count < 1)
         return fail(MEP_EINVAL, "no candidates for this call");
     const int saved = variant_of(call->op);
@@ -1320,7 +1367,8 @@ int mep_select_variant(const mep_call_t* call, int warmup, int R, int k, int inn
         rc = run_and_fetch(call, v == 0 ? base : out);
         if (rc)
             break;
-        r.fe_err = v == 0 ? 0.0 : fe_metric_call(call, out, base);
+        // the baseline is held to its own outputs: 0, or +inf when any is not finite
+        r.fe_err = fe_metric_call(call, v == 0 ? base : out, base);
         r.fe_pass = r.fe_err <= tol ? 1 : 0;
         if (r.fe_pass) {
             rc = mep_time_trimmed(call, warmup, R, k, inner, flush, &r.mean_ms, nullptr);
@@ -1349,6 +1397,9 @@ int mep_check_fe(int dtype, const void* out, const double* ref, int64_t len, dou
         return fail(MEP_EINVAL, "bad arguments to mep_check_fe");
     double worst = 0.0, scale = 0.0;
     bool finite = true;
+    for (int64_t i = 0; i < len; ++i)
+        if (!std::isfinite(ref[i]))
+            return fail(MEP_EINVAL, "reference element %lld is not finite", (long long)i);
     for (int64_t i = 0; i < len; ++i) {
         const double o = dtype == MEP_F32 ? (double)((const float*)out)[i] : ((const double*)out)[i];
         if (!std::isfinite(o))

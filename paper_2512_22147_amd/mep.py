@@ -150,6 +150,41 @@ def _ptr(t) -> int:
     return t.data_ptr() if t.numel() > 0 else None
 
 
+def _matrix(A, name="A"):
+    """(m, n) of a 2-D float32/float64 matrix."""
+    if A is None or A.dim() != 2:
+        raise ValueError(f"{name} must be a 2-D tensor")
+    dtype_code(A.dtype)
+    return int(A.shape[0]), int(A.shape[1])
+
+
+def _like(t, name, length, ref):
+    """Checks that t has `length` elements and ref's dtype and device, before
+    any pointer reaches the C ABI (which only sees addresses and sizes: a
+    short or mistyped buffer would be read or written past its end)."""
+    if t is None:
+        return
+    if t.dtype != ref.dtype:
+        raise ValueError(f"{name} is {t.dtype}, expected {ref.dtype}")
+    if t.numel() != length:
+        raise ValueError(f"{name} has {t.numel()} elements, expected {length}")
+    if t.device != ref.device:
+        raise ValueError(f"{name} is on {t.device}, expected {ref.device}")
+
+
+def _same_shape(t, name, ref):
+    if t is None:
+        return
+    if tuple(t.shape) != tuple(ref.shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(ref.shape)}")
+    _like(t, name, ref.numel(), ref)
+
+
+def _ws_checked(ws, ref):
+    if ws is not None and ws.device != ref.device:
+        raise ValueError(f"ws is on {ws.device}, expected {ref.device}")
+
+
 def _stream(stream) -> int:
     torch = _torch()
     if stream is None:
@@ -160,6 +195,7 @@ def _stream(stream) -> int:
 def _ws(op, A, ws):
     torch = _torch()
     m, n = A.shape
+    _ws_checked(ws, A)
     need = mep_workspace_bytes(op, dtype_code(A.dtype), m, n)
     if ws is None and need > 0:
         ws = torch.empty(need, dtype=torch.uint8, device=A.device)
@@ -180,7 +216,9 @@ def mep_workspace_bytes(op: int, dtype: int, m: int, n: int) -> int:
 
 def mep_matvec(A, x, y=None, ws=None, stream=None):
     """y = A x."""
-    m, n = A.shape
+    m, n = _matrix(A)
+    _like(x, "x", n, A)
+    _like(y, "y", m, A)
     y = _out(A, m, y)
     ws, wsb = _ws(MEP_OP_MATVEC, A, ws)
     _check(lib().mep_matvec(dtype_code(A.dtype), m, n, _ptr(A), _ptr(x), _ptr(y),
@@ -190,7 +228,13 @@ def mep_matvec(A, x, y=None, ws=None, stream=None):
 
 def mep_matvec_t(A, w, z=None, p=None, q=None, ws=None, stream=None):
     """z = A^T w; with p, also q = A p in the same read of A (BICG)."""
-    m, n = A.shape
+    m, n = _matrix(A)
+    _like(w, "w", m, A)
+    _like(z, "z", n, A)
+    _like(p, "p", n, A)
+    _like(q, "q", m, A)
+    if q is not None and p is None:
+        raise ValueError("q is only written with p (the paired product)")
     z = _out(A, n, z)
     if p is not None and q is None:
         q = _out(A, m, None)
@@ -202,7 +246,10 @@ def mep_matvec_t(A, w, z=None, p=None, q=None, ws=None, stream=None):
 
 def mep_ata_x(A, x, y=None, t=None, ws=None, stream=None):
     """y = A^T (A x); t (optional) receives A x."""
-    m, n = A.shape
+    m, n = _matrix(A)
+    _like(x, "x", n, A)
+    _like(y, "y", n, A)
+    _like(t, "t", m, A)
     y = _out(A, n, y)
     ws, wsb = _ws(MEP_OP_ATA_X, A, ws)
     _check(lib().mep_ata_x(dtype_code(A.dtype), m, n, _ptr(A), _ptr(x), _ptr(y), _ptr(t),
@@ -212,7 +259,10 @@ def mep_ata_x(A, x, y=None, t=None, ws=None, stream=None):
 
 def mep_axpby_mv(alpha, A, beta, B, x, y=None, ws=None, stream=None):
     """y = alpha A x + beta B x."""
-    m, n = A.shape
+    m, n = _matrix(A)
+    _same_shape(B, "B", A)
+    _like(x, "x", n, A)
+    _like(y, "y", m, A)
     y = _out(A, m, y)
     ws, wsb = _ws(MEP_OP_AXPBY_MV, A, ws)
     _check(lib().mep_axpby_mv(dtype_code(A.dtype), m, n, float(alpha), _ptr(A), float(beta),
@@ -225,7 +275,11 @@ def mep_gemver(alpha, beta, A, u1, v1, u2, v2, y, z, x=None, w=None, Ahat=None, 
 
     Returns (Ahat, x, w).  Pass ``Ahat=A`` for the in-place update."""
     torch = _torch()
-    m, n = A.shape
+    m, n = _matrix(A)
+    for name, v, ln in (("u1", u1, m), ("v1", v1, n), ("u2", u2, m), ("v2", v2, n), ("y", y, m),
+                        ("z", z, n), ("x", x, n), ("w", w, m)):
+        _like(v, name, ln, A)
+    _same_shape(Ahat, "Ahat", A)
     if Ahat is None:
         Ahat = torch.empty_like(A)
     x = _out(A, n, x)
@@ -240,7 +294,10 @@ def mep_gemver(alpha, beta, A, u1, v1, u2, v2, y, z, x=None, w=None, Ahat=None, 
 def mep_reduce_sum(x, s=None, ws=None, stream=None):
     """s = sum of x (one-element tensor)."""
     torch = _torch()
+    dtype_code(x.dtype)
     n = x.numel()
+    _like(s, "s", 1, x)
+    _ws_checked(ws, x)
     if s is None:
         s = torch.empty(1, dtype=x.dtype, device=x.device)
     need = mep_workspace_bytes(MEP_OP_REDUCE_SUM, dtype_code(x.dtype), 1, n)
@@ -255,6 +312,9 @@ def mep_reduce_sum(x, s=None, ws=None, stream=None):
 def mep_vector_add(a, b, c=None, stream=None):
     """c = a + b."""
     torch = _torch()
+    dtype_code(a.dtype)
+    _like(b, "b", a.numel(), a)
+    _like(c, "c", a.numel(), a)
     if c is None:
         c = torch.empty_like(a)
     _check(lib().mep_vector_add(dtype_code(a.dtype), a.numel(), _ptr(a), _ptr(b), _ptr(c),
@@ -274,13 +334,47 @@ def make_call(op, A, in0=None, in1=None, out0=None, out1=None, B=None, alpha=0.0
         m, n = 1, A.numel()
         in0 = A if in0 is None else in0
         A = None
+        dtype_code(in0.dtype)
+        _like(in0, "in0", n, in0)
+        if op == MEP_OP_REDUCE_SUM:
+            _like(out0, "out0", 1, in0)
+        else:
+            _like(in1, "in1", n, in0)
+            _like(out0, "out0", n, in0)
+        _ws_checked(ws, in0)
         need = mep_workspace_bytes(op, dtype_code(in0.dtype), m, n)
         if ws is None and need > 0:
             ws = torch.empty(need, dtype=torch.uint8, device=in0.device)
         wsb = 0 if ws is None else ws.numel() * ws.element_size()
         dt = dtype_code(in0.dtype)
     else:
-        m, n = A.shape
+        m, n = _matrix(A)
+        # expected lengths of in0.., out0.. per op (None: not used by the op)
+        lengths = {
+            MEP_OP_MATVEC: ({"in0": n}, {"out0": m}),
+            MEP_OP_MATVEC_T: ({"in0": m}, {"out0": n}),
+            MEP_OP_BICG: ({"in0": m, "in1": n}, {"out0": n, "out1": m}),
+            MEP_OP_ATA_X: ({"in0": n}, {"out0": n, "out1": m}),
+            MEP_OP_AXPBY_MV: ({"in0": n}, {"out0": m}),
+            MEP_OP_GEMVER: ({"in0": m, "in1": n, "in2": m, "in3": n, "in4": m, "in5": n},
+                            {"out0": n, "out1": m, "out2": m * n}),
+        }
+        if op not in lengths:
+            raise ValueError(f"unknown op {op}")
+        given = {"in0": in0, "in1": in1, "in2": in2, "in3": in3, "in4": in4, "in5": in5,
+                 "out0": out0, "out1": out1, "out2": out2}
+        ins, outs = lengths[op]
+        for name, t in given.items():
+            want = ins.get(name, outs.get(name))
+            if want is None:
+                if t is not None:
+                    raise ValueError(f"{name} is not used by op {op}")
+            else:
+                _like(t, name, want, A)
+        if op == MEP_OP_AXPBY_MV:
+            _same_shape(B, "B", A)
+        elif B is not None:
+            raise ValueError(f"B is not used by op {op}")
         ws, wsb = _ws(op, A, ws)
         dt = dtype_code(A.dtype)
     c = MepCall()
@@ -396,4 +490,6 @@ def mep_stream_copy(src, dst, stream=None) -> None:
     nbytes = src.numel() * src.element_size()
     if dst.numel() * dst.element_size() < nbytes:
         raise ValueError("dst smaller than src")
+    if dst.device != src.device:
+        raise ValueError(f"dst is on {dst.device}, expected {src.device}")
     _check(lib().mep_stream_copy(_ptr(src), _ptr(dst), nbytes, _stream(stream)))

@@ -1,4 +1,4 @@
-"""Speedup reporting of the MEP loop (Sec. 4.1.3).
+"""Speedup reporting of the MEP loop (Sec. 4.1.4).
 
 The paper scores a kernel by Speedup = t_baseline / t_optimized, with t the
 average (here: the Eq. 3 trimmed mean) execution time, and counts only
@@ -13,7 +13,7 @@ from typing import Iterable, Optional, Sequence
 
 
 def speedup(t_baseline: float, t_optimized: float) -> float:
-    """Speedup = t_baseline / t_optimized (Sec. 4.1.3)."""
+    """Speedup = t_baseline / t_optimized (Sec. 4.1.4)."""
     if not (t_baseline > 0 and t_optimized > 0):
         raise ValueError("times must be positive")
     return t_baseline / t_optimized

@@ -110,9 +110,60 @@ def normwise(out, ref):
     return worst / scale
 
 
-def assert_parity(op, got, ref, dt, what=""):
+def condition_scales(op, ins, dt, alpha=ALPHA, beta=BETA):
+    """Per-element error scales of each output: the same operation on the
+    absolute values of every input (and |alpha|, |beta|), in the oracle --
+    |A| |x| for y = A x, |A|^T (|A| |x|) for ATAX, |alpha| |A| |x| + |beta|
+    |B| |x| for GESUMMV, and so on.  Any summation order of depth d keeps
+    |out_i - exact_i| <= gamma_d * scale_i (first order)."""
+    absins = {k: np.abs(v) for k, v in ins.items()}
+    return oracle_outputs(op, absins, dt, alpha=abs(alpha), beta=abs(beta))
+
+
+def diagnostics(got, ref, scale=None):
+    """(normwise, element-wise relative, condition-scaled) error of one output.
+    Element-wise: max |out_i - ref_i| / |ref_i| over ref_i != 0 (fails even for
+    correct fp32 results near zero, so it is logged only).  Condition-scaled:
+    max |out_i - ref_i| / scale_i (+inf where scale_i = 0 and out_i != ref_i)."""
+    out = np.asarray(got, np.float64).ravel()
+    r = np.asarray(ref, np.float64).ravel()
+    d = np.abs(out - r)
+    nz = r != 0
+    elem = float(np.max(d[nz] / np.abs(r[nz]))) if nz.any() else 0.0
+    cond = None
+    if scale is not None:
+        sc = np.asarray(scale, np.float64).ravel()
+        pos = sc > 0
+        cond = float(np.max(d[pos] / sc[pos])) if pos.any() else 0.0
+        if (d[~pos] > 0).any():
+            cond = float("inf")
+    return normwise(out, r), elem, cond
+
+
+def cond_bound(m, n, dt):
+    """A rigorous bound on the condition-scaled error of any of these
+    operations: no output passes through more than m + n + 64 roundings
+    (a row dot of n terms, a column sum of m, the partial-sum stages and
+    epilogues); twice gamma_d, since the fp64 oracle's own error is of the
+    same order as an fp64 GPU result's."""
+    u = {np.dtype(np.float32): 2.0**-24, np.dtype(np.float64): 2.0**-53}[np.dtype(dt)]
+    d = m + n + 64
+    return 2.0 * d * u / (1.0 - d * u)
+
+
+def assert_parity(op, got, ref, dt, what="", scales=None, dims=None):
+    """Normwise error <= TOL is the pass criterion; the element-wise and
+    condition-scaled errors are printed beside it, and with `scales` (from
+    condition_scales) and `dims` = (m, n) the condition-scaled error must also
+    stay within cond_bound."""
     tol = TOL[dt]
     for k, r in ref.items():
         assert got[k].shape == r.shape, f"{what} {k}: shape {got[k].shape} vs {r.shape}"
-        err = normwise(got[k], r)
-        assert err <= tol, f"{what} {op} {k}: normwise error {err:.3e} > {tol:.0e}"
+        err, elem, cond = diagnostics(got[k], r, None if scales is None else scales[k])
+        print(f"parity {what} {op} {k}: normwise {err:.3e} elementwise {elem:.3e} "
+              f"condition-scaled {'-' if cond is None else f'{cond:.3e}'}")
+        assert err <= tol, (f"{what} {op} {k}: normwise error {err:.3e} > {tol:.0e} "
+                            f"(elementwise {elem:.3e}, condition-scaled {cond})")
+        if cond is not None and dims is not None:
+            bound = cond_bound(dims[0], dims[1], dt)
+            assert cond <= bound, f"{what} {op} {k}: condition-scaled error {cond:.3e} > {bound:.3e}"

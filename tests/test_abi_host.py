@@ -68,6 +68,15 @@ def test_check_fe_matches_metric(dt):
     assert mep.mep_check_fe(np.zeros(4, dt), np.zeros(4), 0.0) == (0.0, True)
     assert mep.mep_check_fe(np.array([0, 1e-30], dt), np.zeros(2), 1.0)[1] is False
     assert mep.mep_check_fe(np.zeros(0, dt), np.zeros(0), 0.0) == (0.0, True)
+    # a non-finite reference is refused: max() would skip a NaN entry, and an
+    # all-NaN reference would otherwise pass every output
+    for v in (np.nan, np.inf):
+        badref = ref.copy()
+        badref[3] = v
+        with pytest.raises(mep.MepError, match="not finite"):
+            mep.mep_check_fe(ref.astype(dt), badref, 1.0)
+    with pytest.raises(mep.MepError):
+        mep.mep_check_fe(np.zeros(4, dt), np.full(4, np.nan), 1.0)
 
 
 def test_workspace_sizes():

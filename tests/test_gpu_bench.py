@@ -47,6 +47,12 @@ def test_bench_json_line_is_consistent():
     cpu = d["cpu_baseline"]
     assert cpu["kind"] == "oracle" and cpu["unit"] == "GB/s" and cpu["value"] > 0 and cpu["cores"] >= 1
     assert d["fe_error_vs_oracle"] <= 1e-4
+    fe = d["fe_vs_oracle"]
+    assert fe["normwise"] == d["fe_error_vs_oracle"] and fe["pass"] is True
+    # the diagnostics beside it: the condition-scaled error is within the
+    # rigorous bound 2 gamma_(m+n+64) of any summation order (~3.9e-3 here)
+    assert 0 <= fe["condition_scaled"] < 2 * (m + n + 64) * 2.0**-24
+    assert fe["elementwise"] >= 0
     assert len(d["other_configs"]) == 4
     for o in d["other_configs"]:
         assert o["ms_per_step"] > 0 and o["kernel_gbs"] > 0 and o["same_size_read_gbs"] > 0

@@ -7,7 +7,7 @@ integer in either precision; bitwise run-to-run reproducibility.
 import numpy as np
 import pytest
 
-from tests.gpu_cases import (OPS, assert_parity, gpu_outputs, make_inputs, op_code,
+from tests.gpu_cases import (OPS, assert_parity, condition_scales, gpu_outputs, make_inputs, op_code,
                              oracle_outputs)
 
 pytestmark = pytest.mark.gpu
@@ -51,13 +51,14 @@ def test_edge_shapes_every_candidate(op, shape, dt):
     m, n = shape
     ins = make_inputs(op, m, n, dt, seed=1000 + m + 7 * n)
     ref = oracle_outputs(op, ins, dt)
+    scales = condition_scales(op, ins, dt)
     code = op_code(op)
     count = mep.mep_variant_count(code, mep.MEP_F32 if dt == np.float32 else mep.MEP_F64, m, n)
     assert count >= 1
     for v in range(count):
         mep.mep_set_variant(code, v)
         got = gpu_outputs(op, ins, dt)
-        assert_parity(op, got, ref, dt, what=f"{m}x{n} candidate {v}")
+        assert_parity(op, got, ref, dt, what=f"{m}x{n} candidate {v}", scales=scales, dims=(m, n))
 
 
 @pytest.mark.parametrize("dt", DTYPES, ids=["f32", "f64"])
@@ -290,8 +291,9 @@ def test_full_size_workloads(name, dts):
     else:
         ins = dict(raw)
     ref = oracle_outputs(op, ins, dt, alpha=w.alpha or 1.5, beta=w.beta or 1.2)
+    scales = condition_scales(op, ins, dt, alpha=w.alpha or 1.5, beta=w.beta or 1.2)
     got = gpu_outputs(op, ins, dt, alpha=w.alpha or 1.5, beta=w.beta or 1.2)
-    assert_parity(op, got, ref, dt, what=name)
+    assert_parity(op, got, ref, dt, what=name, scales=scales, dims=ins["A"].shape)
     if name == "ata_x_16384":
         again = gpu_outputs(op, ins, dt)
         for k in got:
@@ -471,7 +473,8 @@ def test_random_shapes(case):
     ins = make_inputs(op, m, n, dt, seed=7000 + case)
     ref = oracle_outputs(op, ins, dt)
     got = gpu_outputs(op, ins, dt)
-    assert_parity(op, got, ref, dt, what=f"case {case}: {op} {m}x{n} {np.dtype(dt).name}")
+    assert_parity(op, got, ref, dt, what=f"case {case}: {op} {m}x{n} {np.dtype(dt).name}",
+                  scales=condition_scales(op, ins, dt), dims=(m, n))
 
 
 @pytest.mark.parametrize("case", range(len(RANDOM_STREAMED_CASES)))

@@ -1,4 +1,4 @@
-"""Speedup reporting (Sec. 4.1.3) against the averages the paper prints."""
+"""Speedup reporting (Sec. 4.1.4) against the averages the paper prints."""
 import json
 import math
 import os
