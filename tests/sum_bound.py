@@ -4,7 +4,9 @@ its summation depth.
 Any floating-point summation whose longest chain of additions is d satisfies
 |s_computed - s| <= gamma_d * sum_i |x_i|, gamma_d = d u / (1 - d u), with u
 the unit roundoff (Higham, Accuracy and Stability of Numerical Algorithms,
-2nd ed., Sec. 4.2: every term passes through at most d roundings).
+2nd ed., Sec. 4.2: every term passes through at most d roundings).  The
+oracle's reference is itself such a sum (ascending order, d = n - 1, in fp64),
+so the two differ by at most the sum of their bounds.
 
 The sum's order (include/mep.h, mep_reduce_sum): nb workgroups, nb = min(
 ceil(n_v / 8192), 512) with n_v the 16-byte vectors of x (n * esize / 16), each
@@ -38,9 +40,14 @@ def sum_depth(n: int, dt, offset: int = 0) -> int:
     return -(-chunk // 256) + 64
 
 
-def sum_error_bound(n: int, dt, offset: int = 0) -> float:
-    """gamma_d for the sum of n elements of dtype dt: the bound on
-    |s - sum x| / sum |x_i|."""
-    u = UNIT_ROUNDOFF[np.dtype(dt)]
-    d = sum_depth(n, dt, offset)
+def gamma(d: int, u: float) -> float:
     return d * u / (1.0 - d * u) if d * u < 1 else math.inf
+
+
+def sum_error_bound(n: int, dt, offset: int = 0) -> float:
+    """Bound on |s_gpu - s_oracle| / sum |x_i| for the sum of n elements of
+    dtype dt: gamma_d of the GPU's order plus gamma_(n-1) in fp64 of the
+    oracle's own ascending-order sum (which dominates for fp64 inputs: the
+    oracle is not exact either)."""
+    d = sum_depth(n, dt, offset)
+    return gamma(d, UNIT_ROUNDOFF[np.dtype(dt)]) + gamma(max(n - 1, 0), UNIT_ROUNDOFF[np.dtype(np.float64)])

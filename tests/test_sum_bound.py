@@ -17,6 +17,8 @@ def test_depth_of_the_benchmark_sum():
     assert sum_chunks(1 << 28, np.float32) == (512, 1 << 17, 4)
     assert sum_depth(1 << 28, np.float32) == 512 + 64
     assert 3.4e-5 < sum_error_bound(1 << 28, np.float32) < 3.5e-5
+    # fp64: the oracle's own sequential error dominates (gamma_(n-1) in fp64)
+    assert sum_error_bound(1 << 20, np.float64) > (1 << 20) * 2.0**-53
     # the element-wise path (x off a 16-byte boundary) has 4x longer lane chains
     assert sum_depth(1 << 28, np.float32, offset=1) == 2048 + 64
     assert sum_chunks(0, np.float64) == (1, 0, 2)
