@@ -112,6 +112,26 @@ int mep_ata_x(int dtype, int64_t m, int64_t n, const void* A, const void* x, voi
               void* t, void* ws, size_t ws_bytes, mep_stream_t stream);
 
 /*
+ * Allocation-free variant of mep_ata_x, for callers that cannot allocate or
+ * bring workspace: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation.  The same kernels and results as
+ * mep_ata_x (bit for bit), with the column partials kept in a scratch array
+ * that the library owns on each GPU: MEP_NOALLOC_SCRATCH_BYTES (64 MiB),
+ * reserved on a device when the library's code is first loaded there and
+ * held until the process ends; its address is looked up on the first call on
+ * a device.  The call allocates and frees nothing.  A call whose plan needs
+ * more scratch than that (e.g. a row too long to keep on chip, which takes
+ * the two-pass path over a huge m) returns MEP_EWORKSPACE and launches
+ * nothing.  Every call on one GPU shares that GPU's scratch: calls that may
+ * overlap on one GPU (other streams, other host threads) race and must be
+ * serialized by the caller.  The device is the stream's (the current
+ * device for a NULL stream).  Arguments as for mep_ata_x, without ws.
+ */
+#define MEP_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+int mep_ata_x_noalloc(int dtype, int64_t m, int64_t n, const void* A, const void* x, void* y,
+                      void* t, mep_stream_t stream);
+
+/*
  * y = alpha A x + beta B x: the GESUMMV kernel of Tables 1-2.  A, B: m x n,
  * x: n, y: m.  On the fp32 path alpha and beta are rounded to fp32 first.
  */

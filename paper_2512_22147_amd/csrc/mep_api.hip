@@ -11,6 +11,7 @@
 #include <cstdio>
 #include <cstring>
 #include <limits>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -641,6 +642,22 @@ static int run_matvec_t(int64_t m, int64_t n, const T* A, const T* w, T* z, cons
     return e == hipSuccess ? MEP_OK : hip_fail(e, "matvec_t launch");
 }
 
+// Workspace bytes the ATAX call with these operands really uses (the plan
+// of the op's current variant; mep_workspace_bytes covers every candidate).
+static size_t ata_x_used_bytes(int esize, bool vec, int64_t m, int64_t n)
+{
+    if (m == 0 || n == 0)
+        return 0;
+    const int variant = g_variant[MEP_OP_ATA_X].load(std::memory_order_relaxed);
+    const Plan p = plan_stream(esize, vec, MODE_ATAX, m, n, variant);
+    if (p.panels == 1)
+        return layout_for(MODE_ATAX, p, esize, m, n, false).total;
+    const Plan p1 = plan_stream(esize, vec, MODE_MV, m, n, variant);
+    const Plan p2 = plan_stream(esize, vec, MODE_ATW, m, n, variant);
+    const WsLayout l1 = layout_for(MODE_MV, p1, esize, m, n, true);
+    return l1.dotpart + l1.tvec + layout_for(MODE_ATW, p2, esize, m, n, false).colpart;
+}
+
 template <typename T>
 static int run_ata_x(int64_t m, int64_t n, const T* A, const T* x, T* y, T* t, char* ws, hipStream_t s)
 {
@@ -992,6 +1009,91 @@ int mep_ata_x(int dtype, int64_t m, int64_t n, const void* A, const void* x, voi
     if ((rc = check_overlaps(outs, 2, ins, 3)))
         return rc;
     hipStream_t s = (hipStream_t)stream;
+    if (dtype == MEP_F32)
+        return run_ata_x<float>(m, n, (const float*)A, (const float*)x, (float*)y, (float*)t, (char*)ws, s);
+    return run_ata_x<double>(m, n, (const double*)A, (const double*)x, (double*)y, (double*)t, (char*)ws, s);
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// scratch of the allocation-free ATAX entry point
+// ---------------------------------------------------------------------------
+
+namespace mep {
+
+// Device scratch owned by the library: every GPU that runs the entry point
+// holds its own copy for the life of the process.  Host code never uses the
+// array's name as an address (on the host it is only a stand-in symbol): it
+// takes each device's address once from hipGetSymbolAddress and passes that.
+constexpr size_t kNoAllocScratchBytes = MEP_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mu;
+static void* g_scratch_ptr[kMaxDevices] = {};
+
+// Address of `scratch` on device `dev`, looked up on the first call there
+// (with that device current) and kept.
+static int scratch_on(int dev, void** out)
+{
+    if (dev < 0 || dev >= kMaxDevices)
+        return fail(MEP_EINVAL, "device %d outside 0..%d", dev, kMaxDevices - 1);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_ptr[dev] == nullptr) {
+        int cur = -1;
+        hipError_t e = hipGetDevice(&cur);
+        if (e == hipSuccess && cur != dev)
+            e = hipSetDevice(dev);
+        void* ptr = nullptr;
+        if (e == hipSuccess)
+            e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        const hipError_t back = (cur >= 0 && cur != dev) ? hipSetDevice(cur) : hipSuccess;
+        if (e != hipSuccess)
+            return hip_fail(e, "scratch address");
+        if (back != hipSuccess)
+            return hip_fail(back, "restore device");
+        if (ptr == nullptr)
+            return fail(MEP_EHIP, "scratch address is NULL");
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = g_scratch_ptr[dev];
+    return MEP_OK;
+}
+
+}  // namespace mep
+
+extern "C" {
+
+int mep_ata_x_noalloc(int dtype, int64_t m, int64_t n, const void* A, const void* x, void* y, void* t,
+                      mep_stream_t stream)
+{
+    int rc = check_sizes(dtype, m, n);
+    if (rc)
+        return rc;
+    const int es = esize_of(dtype);
+    if ((rc = check_ptr(A, m * n, es, "A")) || (rc = check_ptr(x, n, es, "x")) ||
+        (rc = check_ptr(y, n, es, "y")))
+        return rc;
+    if (t != nullptr && (rc = check_ptr(t, m, es, "t")))
+        return rc;
+    const bool vec = vec_ok_n(es, n) && aligned(A, 16) && aligned(x, 16);
+    const size_t need = ata_x_used_bytes(es, vec, m, n);
+    if (need > kNoAllocScratchBytes)
+        return fail(MEP_EWORKSPACE, "this call needs %zu bytes of scratch; the allocation-free entry point "
+                    "holds %zu (use mep_ata_x with a workspace)", need, kNoAllocScratchBytes);
+    const Range outs[] = {{y, (size_t)n * es, "y"}, {t, t ? (size_t)m * es : 0, "t"}};
+    const Range ins[] = {{A, (size_t)(m * n) * es, "A"}, {x, (size_t)n * es, "x"}};
+    if ((rc = check_overlaps(outs, 2, ins, 2)))
+        return rc;
+    hipStream_t s = (hipStream_t)stream;
+    int dev = -1;
+    hipError_t e = s != nullptr ? hipStreamGetDevice(s, &dev) : hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return hip_fail(e, "stream device");
+    void* ws = nullptr;
+    if ((rc = scratch_on(dev, &ws)))
+        return rc;
     if (dtype == MEP_F32)
         return run_ata_x<float>(m, n, (const float*)A, (const float*)x, (float*)y, (float*)t, (char*)ws, s);
     return run_ata_x<double>(m, n, (const double*)A, (const double*)x, (double*)y, (double*)t, (char*)ws, s);

@@ -31,7 +31,9 @@ EXPORTS = (
     "mep_variant_count", "mep_set_variant", "mep_variant_info", "mep_profile_begin", "mep_profile_end",
     "mep_stream_copy", "mep_last_error", "mep_version", "mep_select_variant",
     "mep_reduce_sum", "mep_vector_add", "mep_gemver", "mep_profile_end_samples", "mep_profile_begin_sampled",
+    "mep_ata_x_noalloc",
 )
+NOALLOC_SCRATCH_BYTES = 64 << 20  # MEP_NOALLOC_SCRATCH_BYTES
 
 
 class MepError(RuntimeError):
@@ -81,6 +83,7 @@ def lib() -> ctypes.CDLL:
     L.mep_matvec_t.argtypes = [i, i64, i64, vp, vp, vp, vp, vp, vp, sz, vp]
     L.mep_ata_x.argtypes = [i, i64, i64, vp, vp, vp, vp, vp, sz, vp]
     L.mep_axpby_mv.argtypes = [i, i64, i64, d, vp, d, vp, vp, vp, vp, sz, vp]
+    L.mep_ata_x_noalloc.argtypes = [i, i64, i64, vp, vp, vp, vp, vp]
     L.mep_run.argtypes = [ctypes.POINTER(MepCall)]
     L.mep_time_trimmed.argtypes = [ctypes.POINTER(MepCall), i, i, i, i, i,
                                    ctypes.POINTER(d), ctypes.POINTER(d)]
@@ -254,6 +257,21 @@ def mep_ata_x(A, x, y=None, t=None, ws=None, stream=None):
     ws, wsb = _ws(MEP_OP_ATA_X, A, ws)
     _check(lib().mep_ata_x(dtype_code(A.dtype), m, n, _ptr(A), _ptr(x), _ptr(y), _ptr(t),
                            _ptr(ws), wsb, _stream(stream)))
+    return y
+
+
+def mep_ata_x_noalloc(A, x, y, t=None, stream=None):
+    """y = A^T (A x) through the allocation-free entry point: the caller
+    passes every output (y, and t if wanted); the library's own per-GPU
+    scratch replaces the workspace.  Calls that overlap on one GPU race."""
+    m, n = _matrix(A)
+    _like(x, "x", n, A)
+    if y is None:
+        raise ValueError("y must be given: this entry point allocates nothing")
+    _like(y, "y", n, A)
+    _like(t, "t", m, A)
+    _check(lib().mep_ata_x_noalloc(dtype_code(A.dtype), m, n, _ptr(A), _ptr(x), _ptr(y), _ptr(t),
+                                   _stream(stream)))
     return y
 
 

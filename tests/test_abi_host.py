@@ -32,7 +32,7 @@ def L():
 
 def test_library_exports_every_declared_function(L):
     names = declared_functions()
-    assert len(names) == 23
+    assert len(names) == 24
     for name in names:
         assert hasattr(L, name), f"{name} not exported"
     assert sorted(mep.EXPORTS) == names
@@ -305,3 +305,18 @@ def test_harness_errors(L):
     c.flush_buf, c.flush_bytes = None, 0
     c.op = 77
     assert L.mep_select_variant(ctypes.byref(c), 0, 30, 3, 1, 0, 1e-4, 0, ctypes.byref(best), None, 0) == mep.MEP_EINVAL
+
+
+def test_noalloc_refuses_beyond_its_scratch_before_any_launch(L):
+    """mep_ata_x_noalloc checks its plan's scratch need before touching a
+    device: 2^23 rows of 40000 fp32 (two-pass path) need more than 64 MiB.
+    The pointers are never dereferenced."""
+    import ctypes
+
+    base = 1 << 40
+    rc = L.mep_ata_x_noalloc(mep.MEP_F32, 1 << 23, 40000, ctypes.c_void_p(base),
+                             ctypes.c_void_p(base + (1 << 42)), ctypes.c_void_p(base + (1 << 43)), None, None)
+    assert rc == mep.MEP_EWORKSPACE
+    assert str(mep.NOALLOC_SCRATCH_BYTES) in mep.mep_last_error()
+    assert L.mep_ata_x_noalloc(mep.MEP_F32, 4, 4, None, None, None, None, None) == mep.MEP_EINVAL
+    assert L.mep_ata_x_noalloc(9, 4, 4, None, None, None, None, None) == mep.MEP_EINVAL

@@ -1,0 +1,83 @@
+"""The allocation-free ATAX entry point (mep_ata_x_noalloc) through the C ABI:
+the same results as mep_ata_x, bit for bit and within the oracle tolerance,
+on two calls in a row whose second input is smaller (the scratch keeps the
+first call's contents), for both element types; a call whose plan needs more
+than the scratch holds is refused before anything is written."""
+import ctypes
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2512_22147_amd import datagen, mep
+from tests.gpu_cases import TOL, normwise
+
+pytestmark = pytest.mark.gpu
+
+# (first call, second smaller call) per element type; the first is the
+# benchmark's fp32 matrix or a streamed fp64 one, the second ragged
+CASES = {np.float32: [(16384, 16384), (1500, 2052)], np.float64: [(6000, 8192), (301, 516)]}
+
+
+@pytest.fixture(autouse=True)
+def _gpu():
+    import torch
+
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    mep.mep_set_variant(mep.MEP_OP_ATA_X, -1)
+    yield
+    mep.mep_set_variant(mep.MEP_OP_ATA_X, -1)
+
+
+def _raw_noalloc(dt, A, x, y, t):
+    """The C entry point itself (no binding logic in between)."""
+    import torch
+
+    L = mep.lib()
+    code = mep.MEP_F32 if dt == np.float32 else mep.MEP_F64
+    m, n = A.shape
+    return L.mep_ata_x_noalloc(code, m, n, ctypes.c_void_p(A.data_ptr()), ctypes.c_void_p(x.data_ptr()),
+                               ctypes.c_void_p(y.data_ptr()), ctypes.c_void_p(t.data_ptr()),
+                               ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+
+
+@pytest.mark.parametrize("dt", [np.float32, np.float64], ids=["f32", "f64"])
+def test_noalloc_matches_the_workspace_entry_point(dt):
+    import torch
+
+    dev = torch.device("cuda:0")
+    tdt = torch.float32 if dt == np.float32 else torch.float64
+    for call, (m, n) in enumerate(CASES[dt]):
+        print(f"noalloc {np.dtype(dt).name} call {call}: {m}x{n}", flush=True)
+        Ah = datagen.uniform(40 + call, 0, (m, n), dt)
+        xh = datagen.uniform(40 + call, 1, (n,), dt)
+        A = torch.from_numpy(Ah).to(dev)
+        x = torch.from_numpy(xh).to(dev)
+        guard = 1024
+        y_all = torch.full((n + guard,), 555.0, dtype=tdt, device=dev)
+        t_all = torch.full((m + guard,), 555.0, dtype=tdt, device=dev)
+        y, t = y_all[:n], t_all[:m]
+        assert _raw_noalloc(dt, A, x, y, t) == mep.MEP_OK, mep.mep_last_error()
+        t_ref = torch.empty(m, dtype=tdt, device=dev)
+        y_ref = mep.mep_ata_x(A, x, t=t_ref)
+        torch.cuda.synchronize()
+        assert torch.equal(y, y_ref) and torch.equal(t, t_ref), f"call {call}: differs from mep_ata_x"
+        assert bool((y_all[n:] == 555.0).all()) and bool((t_all[m:] == 555.0).all()), "wrote past an output"
+        ref_y, ref_t = oracle.ata_x(Ah, xh)
+        assert normwise(y.cpu().numpy(), ref_y) <= TOL[dt]
+        assert normwise(t.cpu().numpy(), ref_t) <= TOL[dt]
+        del A, x, y_all, t_all, t_ref, y_ref
+        torch.cuda.empty_cache()
+
+
+def test_noalloc_refuses_a_plan_beyond_its_scratch():
+    """Rows past the on-chip width take the two-pass path; with 2^23 rows of
+    40000 fp32 its partial dots, t and column partials exceed 64 MiB.  The
+    pointers are never dereferenced: the size check comes first."""
+    L = mep.lib()
+    fake = ctypes.c_void_p(1 << 40)
+    rc = L.mep_ata_x_noalloc(mep.MEP_F32, 1 << 23, 40000, fake, ctypes.c_void_p((1 << 40) + (1 << 42)),
+                             ctypes.c_void_p((1 << 40) + (1 << 43)), None, None)
+    assert rc == mep.MEP_EWORKSPACE
+    assert "64" in mep.mep_last_error() or str(mep.NOALLOC_SCRATCH_BYTES) in mep.mep_last_error()
