@@ -96,6 +96,8 @@ def parse():
                          "the chosen shape's standalone speedup over the default (Sec. 4.1.4)")
     ap.add_argument("--no-eq3", action="store_true",
                     help="skip the Eq. 3 cold-cache timing (R = 30, k = 3, 1 GiB flush per sample)")
+    ap.add_argument("--probe-floor", action="store_true",
+                    help="also time back-to-back launches of a 16-byte copy (the launch floor)")
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the step timing of the other benchmark configurations (reported beside "
                          "the headline as other_configs)")
@@ -263,7 +265,11 @@ def select_round(workload: str, dtype: str):
     best, res = mep.mep_select_variant(call, warmup=EQ3["warmup"], R=EQ3["R"], k=EQ3["k"], flush=True,
                                        tol=tol, apply=False)
     dt = mep.dtype_code(S["tdt"])
-    out = {"candidates": len(res), "fe_passed": sum(1 for r in res if r[2]), "best": best,
+    per = [{"candidate": i, "config": mep.mep_variant_info(S["code"], dt, S["m"], S["n"], i),
+            "trimmed_mean_ms": None if r[0] != r[0] else round(r[0], 5), "fe_err": float(f"{r[1]:.3g}"),
+            "fe_pass": r[2]} for i, r in enumerate(res)]
+    out = {"workload": workload, "dtype": dtype, "per_candidate": per,
+           "candidates": len(res), "fe_passed": sum(1 for r in res if r[2]), "best": best,
            "best_config": mep.mep_variant_info(S["code"], dt, S["m"], S["n"], max(best, 0)),
            "baseline_config": mep.mep_variant_info(S["code"], dt, S["m"], S["n"], 0),
            "baseline_ms": round(res[0][0], 5), "best_ms": round(res[best][0], 5) if best >= 0 else None,
@@ -277,7 +283,37 @@ def select_round(workload: str, dtype: str):
 PROFILE_EVERY = 8
 
 
-def run_gpu(workload: str, dtype: str, steps: int, warmup: int, variant: int, eq3_flush: bool = True):
+def graph_step_ms(S, steps: int) -> float:
+    """Device time per step with the host out of the way: the K steps are
+    captured into one HIP graph (the operations only enqueue kernels) and the
+    graph is replayed once untimed, then once timed between two device
+    synchronizations.  Small workloads finish a step in less time than Python
+    takes to issue one, so eager timing would measure the host."""
+    import torch
+
+    from paper_2512_22147_amd import mep
+
+    call = S["call"]
+    saved = call.stream
+    s = torch.cuda.Stream()
+    call.stream = s.cuda_stream
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        for _ in range(steps):
+            mep.mep_run(call)
+    g.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    g.replay()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    call.stream = saved
+    del g
+    return elapsed * 1e3 / steps
+
+
+def run_gpu(workload: str, dtype: str, steps: int, warmup: int, variant: int, eq3_flush: bool = True,
+            graph: bool = False):
     import torch
 
     from paper_2512_22147_amd import mep
@@ -306,6 +342,9 @@ def run_gpu(workload: str, dtype: str, steps: int, warmup: int, variant: int, eq
     samples, kern_ms, launches = mep.mep_profile_end_samples(stamped * len(kern) + 16)
     config = mep.mep_variant_info(code, mep.dtype_code(S["tdt"]), S["m"], S["n"], max(variant, 0))
     ms_step = elapsed * 1e3 / steps
+    ms_eager = ms_step
+    if graph:
+        ms_step = graph_step_ms(S, steps)
     eq3 = eq3_timing(S, ms_step) if eq3_flush else None
     mep.mep_set_variant(code, -1)
     per_kernel = []
@@ -321,7 +360,7 @@ def run_gpu(workload: str, dtype: str, steps: int, warmup: int, variant: int, eq
         dom = {"kernel": kern[0][0], "ms": kern_ms / max(launches, 1), "alg_bytes": kern[0][1]}
         dom["gbs"] = dom["alg_bytes"] / (dom["ms"] * 1e-3) / 1e9
     res = {
-        "dtype": dtype, "m": S["m"], "n": S["n"], "ms_per_step": ms_step,
+        "dtype": dtype, "m": S["m"], "n": S["n"], "ms_per_step": ms_step, "ms_per_step_eager": ms_eager,
         "value_gbs": S["alg_step"] / (ms_step * 1e-3) / 1e9,
         "kernel_ms": dom["ms"], "kernel_launches": launches, "kernel_name": dom["kernel"],
         "kernel_gbs": dom["gbs"], "per_kernel": per_kernel if len(per_kernel) > 1 else None,
@@ -355,6 +394,50 @@ def probe_copy():
     log(f"[bench] copy probe: {nbytes} B read + {nbytes} B written per launch, "
         f"{2 * nbytes / dt / 1e9:.1f} GB/s")
     return {"bytes_read": nbytes, "bytes_written": nbytes, "gbs": 2 * nbytes / dt / 1e9}
+
+
+def probe_floor(reps: int = 200):
+    """The launch floor: `reps` launches of a 16-byte mep_stream_copy (one
+    workgroup; one load and one store by the lane that has data) captured into
+    one HIP graph and replayed, so that the host is out of the way; the time
+    per launch is what any extra kernel of a step costs at least."""
+    import torch
+
+    from paper_2512_22147_amd import mep
+
+    dev = torch.device("cuda:0")
+    src = torch.ones(16, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    s = torch.cuda.Stream()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        for _ in range(reps):
+            mep.mep_stream_copy(src, dst, stream=s)
+    g.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    g.replay()
+    torch.cuda.synchronize()
+    us = (time.perf_counter() - t0) * 1e6 / reps
+    log(f"[bench] launch floor: {us:.2f} us per launch of a 16-byte copy (graph replay)")
+    del g
+    return {"kernel": "k_copy16 (16 bytes, one workgroup)", "launches": reps, "timing": "graph replay",
+            "us_per_launch": round(us, 3)}
+
+
+def mix_ceiling(read_gbs: float, copy_gbs: float, bytes_read: int, bytes_written: int):
+    """Bandwidth bound of a kernel that reads R and writes W bytes, from the
+    measured read ceiling and copy rate: the copy gives the time a written byte
+    costs beside a read one (t_copy = N / read + N / write), and the kernel's
+    bound is (R + W) / (R / read + W / write)."""
+    t_read_byte = 1.0 / (read_gbs * 1e9)
+    t_write_byte = 2.0 / (copy_gbs * 1e9) - t_read_byte
+    if t_write_byte <= 0:
+        return None
+    t = bytes_read * t_read_byte + bytes_written * t_write_byte
+    return {"read_gbs": read_gbs, "copy_gbs": copy_gbs, "write_gbs_derived": round(1.0 / t_write_byte / 1e9, 1),
+            "bytes_read": bytes_read, "bytes_written": bytes_written,
+            "mix_gbs": round((bytes_read + bytes_written) / t / 1e9, 1)}
 
 
 def cpu_model() -> str:
@@ -544,19 +627,38 @@ def main():
     if args.workload == HEADLINE and not args.no_configs:
         others = []
         for wl, dt in OTHER_CONFIGS:
-            r = run_gpu(wl, dt, args.steps, args.warmup, -1, False)
+            r = run_gpu(wl, dt, args.steps, args.warmup, -1, False, graph=True)
             # a plain read of as many matrix bytes, from wherever they live
             # (HBM, or the Infinity Cache for matrices of at most 128 MiB)
             mats = 2 if r["w"].op == "axpby_mv" else 1
             read_gbs = probe_read(mats * r["m"] * r["n"], dt)
             others.append({
                 "workload": wl, "dtype": dt, "m": r["m"], "n": r["n"],
-                "ms_per_step": round(r["ms_per_step"], 5), "value": round(r["value_gbs"], 1), "unit": "GB/s",
+                "ms_per_step": round(r["ms_per_step"], 5), "timing": "graph replay of the timed steps",
+                "ms_per_step_eager": round(r["ms_per_step_eager"], 5),
+                "value": round(r["value_gbs"], 1), "unit": "GB/s",
                 "kernel_gbs": round(r["kernel_gbs"], 1), "kernel_frac": round(r["kernel_gbs"] / PEAK_GBS, 4),
                 "kernel_config": r["config"], "same_size_read_gbs": round(read_gbs, 1),
                 "kernel_frac_of_read": round(r["kernel_gbs"] / read_gbs, 4),
             })
-    copy = probe_copy() if args.probe_copy else None
+    w0 = datagen.WORKLOADS[args.workload]
+    # kernels that write as much as they read are bound by the read/write mix:
+    # GEMVER's first pass (A read, Ahat written) and the vector add (2:1)
+    mixed = w0.op in ("gemver", "vector_add")
+    copy = probe_copy() if (args.probe_copy or mixed) else None
+    floor = probe_floor() if args.probe_floor else None
+    mix = None
+    if mixed and ceiling is not None and copy is not None:
+        es = 4 if args.dtype == "f32" else 8
+        m_, n_ = prim["m"], prim["n"]
+        if w0.op == "gemver":
+            # pass 1: A, u1, u2, y read once, v1, v2 from L2; Ahat and the partials written
+            rd, wr = (m_ * n_ + 3 * m_ + 2 * n_) * es, m_ * n_ * es
+        else:
+            rd, wr = 2 * n_ * es, n_ * es
+        mix = mix_ceiling(ceiling["gbs"], copy["gbs"], rd, wr)
+        if mix is not None:
+            mix["kernel_frac_of_mix_ceiling"] = round(prim["kernel_gbs"] / mix["mix_gbs"], 4)
     selection = select_round(args.workload, args.dtype) if args.select else None
     w = prim["w"]
     desc = OPS[w.op][2]
@@ -597,6 +699,8 @@ def main():
         "secondary": secondary,
         "other_configs": others,
         "copy_probe": copy,
+        "launch_floor": floor,
+        "mix_ceiling": mix,
         "hbm_ceiling_probe": ceiling,
         "mep_budget": mep_budget(w, args.dtype, prim["kernel_ms"], t_mep),
         "kernel_frac_of_ceiling": None if ceiling is None else round(prim["kernel_gbs"] / ceiling["gbs"], 4),

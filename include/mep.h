@@ -335,9 +335,10 @@ int mep_profile_end(double* total_ms, int* launches);
 int mep_profile_end_samples(double* samples_ms, int cap, double* total_ms, int* launches);
 
 /*
- * Plain device copy of `bytes` bytes (16-byte vector loads and stores):
- * the streaming ceiling probe used to calibrate memory-traffic counters and
- * achievable bandwidth.  src and dst must be 16-byte aligned, must not
+ * Plain device copy of `bytes` bytes (16-byte non-temporal loads and stores,
+ * rows of 64 KiB streamed by up to 256 workgroups): the probe of the
+ * read/write-mix ceiling (one byte written per byte read) and of the traffic
+ * counters' calibration.  src and dst must be 16-byte aligned, must not
  * overlap, and bytes must be a multiple of 16.
  */
 int mep_stream_copy(const void* src, void* dst, size_t bytes, mep_stream_t stream);

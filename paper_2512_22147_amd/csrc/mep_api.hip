@@ -750,24 +750,53 @@ static int run_axpby(int64_t m, int64_t n, T alpha, const T* A, T beta, const T*
 // streaming copy (ceiling probe) and cache flush
 // ---------------------------------------------------------------------------
 
-constexpr int kCopyUnroll = 4;
+// The copy probe streams rows of THREADS * V 16-byte vectors (128 KiB):
+// workgroup w takes rows w, w + gridDim.x, ..., with non-temporal buffer
+// loads and stores (the resource's range check drops the ragged end), the
+// next row loaded while the current one is stored -- the access pattern of
+// the matrix kernels' store pass, without the arithmetic.
+constexpr int kCopyThreads = 1024, kCopyV = 8;
 
-__global__ void __launch_bounds__(256) k_copy16(const uint4* __restrict__ src, uint4* __restrict__ dst,
-                                                int64_t count)
+__global__ void __launch_bounds__(kCopyThreads) k_copy16(const void* __restrict__ src, void* __restrict__ dst,
+                                                         int64_t count)
 {
-    const int64_t stride = (int64_t)gridDim.x * 256;
-    int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    for (; i + (kCopyUnroll - 1) * stride < count; i += kCopyUnroll * stride) {
-        uint4 v[kCopyUnroll];
+    typedef float vec __attribute__((ext_vector_type(4)));
+    constexpr int64_t RV = (int64_t)kCopyThreads * kCopyV;
+    const int64_t rows = (count + RV - 1) / RV;
+    const int tid = threadIdx.x;
+    vec a[kCopyV], b[kCopyV];
+    // one resource per row: base = the row's first vector, size = what is left
+    auto rsrc = [&](const void* base, int64_t r) __attribute__((always_inline)) {
+        const int64_t left = r < rows ? (count - r * RV) * 16 : 0;
+        return make_rsrc(static_cast<const char*>(base) + (r < rows ? r * RV * 16 : 0),
+                         (uint32_t)(left < RV * 16 ? left : RV * 16));
+    };
+    auto load = [&](int64_t r, vec (&v)[kCopyV]) __attribute__((always_inline)) {
+        const __amdgpu_buffer_rsrc_t rs = rsrc(src, r);
 #pragma unroll
-        for (int u = 0; u < kCopyUnroll; ++u)
-            v[u] = src[i + u * stride];
+        for (int k = 0; k < kCopyV; ++k)
+            v[k] = load_buf<float, 4, 2>(rs, (uint32_t)((k * kCopyThreads + tid) * 16), 0);
+    };
+    auto store = [&](int64_t r, vec (&v)[kCopyV]) __attribute__((always_inline)) {
+        const __amdgpu_buffer_rsrc_t rs = rsrc(dst, r);
 #pragma unroll
-        for (int u = 0; u < kCopyUnroll; ++u)
-            dst[i + u * stride] = v[u];
+        for (int k = 0; k < kCopyV; ++k)
+            store_buf<float, 4, 2>(v[k], rs, (uint32_t)((k * kCopyThreads + tid) * 16));
+    };
+    const int64_t step = gridDim.x;
+    int64_t r = blockIdx.x;
+    if (r < rows)
+        load(r, a);
+    while (r < rows) {
+        load(r + step, b);
+        store(r, a);
+        r += step;
+        if (r >= rows)
+            break;
+        load(r + step, a);
+        store(r, b);
+        r += step;
     }
-    for (; i < count; i += stride)
-        dst[i] = src[i];
 }
 
 __global__ void __launch_bounds__(256) k_flush16(uint4* __restrict__ dst, int64_t count, uint32_t tag)
@@ -779,9 +808,9 @@ __global__ void __launch_bounds__(256) k_flush16(uint4* __restrict__ dst, int64_
 hipError_t launch_copy16(const void* src, void* dst, size_t bytes, hipStream_t s)
 {
     const int64_t count = (int64_t)(bytes / 16);
-    const int64_t blocks = std::min<int64_t>((count + 255) / 256, 256 * 16);
-    hipLaunchKernelGGL(k_copy16, dim3((unsigned)blocks), dim3(256), 0, s, (const uint4*)src, (uint4*)dst,
-                       count);
+    const int64_t rv = (int64_t)kCopyThreads * kCopyV;
+    const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>((count + rv - 1) / rv, kXcds * kCusPerXcd));
+    hipLaunchKernelGGL(k_copy16, dim3((unsigned)blocks), dim3(kCopyThreads), 0, s, src, dst, count);
     return hipGetLastError();
 }
 

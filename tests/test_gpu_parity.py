@@ -484,3 +484,23 @@ def test_random_streamed_shapes(case):
     ref = oracle_outputs(op, ins, dt)
     got = gpu_outputs(op, ins, dt)
     assert_parity(op, got, ref, dt, what=f"streamed case {case}: {op} {m}x{n} {np.dtype(dt).name}")
+
+
+@pytest.mark.parametrize("nbytes", [16, 48, (128 << 10) + 16, (3 << 20) + 48, 64 << 20, (1 << 30) + 4096])
+def test_stream_copy_sizes(nbytes):
+    """The copy probe copies every byte, ragged last row included, and
+    writes nothing past dst."""
+    import torch
+
+    from paper_2512_22147_amd import mep
+
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev)
+    g.manual_seed(nbytes % 1000)
+    src = torch.randint(0, 256, (nbytes,), dtype=torch.uint8, device=dev, generator=g)
+    guard = 4096
+    dst_all = torch.full((nbytes + guard,), 0xA5, dtype=torch.uint8, device=dev)
+    mep.mep_stream_copy(src, dst_all[:nbytes])
+    torch.cuda.synchronize()
+    assert torch.equal(src, dst_all[:nbytes])
+    assert bool((dst_all[nbytes:] == 0xA5).all())
