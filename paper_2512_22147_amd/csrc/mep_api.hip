@@ -929,11 +929,14 @@ int mep_variant_info(int op, int dtype, int64_t m, int64_t n, int variant, char*
         if (op == MEP_OP_REDUCE_SUM)
             snprintf(buf, buf_len, "reduce threads=256 grid=%lld, fixed-order partials",
                      (long long)reduce_blocks(n, es));
-        else if (variant == 0)
+        else if (variant < 2)
+            snprintf(buf, buf_len, "vector-add buffer rows threads=1024 V=4 cus=%d/%d, 16-byte non-temporal",
+                     variant == 0 ? kCusPerXcd : 24, kCusPerXcd);
+        else if (variant == 2)
             snprintf(buf, buf_len, "vector-add chunks threads=256, 16-byte non-temporal");
         else
             snprintf(buf, buf_len, "vector-add rows threads=1024 V=4 cus=%d/%d, 16-byte non-temporal",
-                     variant == 1 ? kCusPerXcd : (variant == 2 ? 24 : 16), kCusPerXcd);
+                     variant == 3 ? kCusPerXcd : (variant == 4 ? 24 : 16), kCusPerXcd);
         return MEP_OK;
     }
     const int mode = op_mode(op);

@@ -175,10 +175,11 @@ template <>
 hipError_t launch_vector_add<double>(const double*, const double*, double*, int64_t, int, hipStream_t,
                                      const LaunchEvents&);
 
-// Candidate launches of the vector add: 0 = contiguous chunk per workgroup,
-// 1-3 = row-streamed with 1024-lane workgroups on 32, 24 or 16 compute units
-// per XCD.
-constexpr int kNumVaddVariants = 4;
+// Candidate launches of the vector add: 0-1 = rows of 1024-lane workgroups
+// through buffer resources on 32 or 24 compute units per XCD (0, the
+// default, measured the fastest), 2 = contiguous chunk per workgroup, 3-5 =
+// rows with plain non-temporal loads and stores on 32, 24 or 16.
+constexpr int kNumVaddVariants = 6;
 
 hipError_t launch_copy16(const void* src, void* dst, size_t bytes, hipStream_t s);
 hipError_t launch_flush(void* buf, size_t bytes, uint32_t tag, hipStream_t s);

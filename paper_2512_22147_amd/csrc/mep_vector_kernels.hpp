@@ -148,4 +148,63 @@ k_vector_add_rows(const T* __restrict__ a, const T* __restrict__ b, T* __restric
     }
 }
 
+// c = a + b, row-streamed through buffer resources: as k_vector_add_rows
+// (rows of THREADS * V vectors of each input, row w, w + gridDim.x, ... per
+// workgroup, the next row loaded while the current one is added and stored),
+// but every access is a non-temporal buffer load or store through a
+// resource whose base is the row's first element and whose size is what is
+// left of the vector: one 32-bit offset per lane, the range check drops the
+// ragged end, and the prefetch past the last row reads nothing.
+template <typename T, int VW, int V, int THREADS>
+__global__ void __launch_bounds__(THREADS)
+k_vector_add_buf(const T* __restrict__ a, const T* __restrict__ b, T* __restrict__ c, int64_t n)
+{
+    typedef typename VecOf<T, VW>::type vec;
+    constexpr int64_t RE = (int64_t)THREADS * V * VW;  // elements per row
+    constexpr uint32_t VB = VW * sizeof(T);
+    const int64_t nv = n / VW;
+    const int64_t ne = nv * VW;  // elements covered by whole vectors
+    const int64_t rows = (ne + RE - 1) / RE;
+    const int tid = threadIdx.x;
+    vec xa[V], xb[V], ya[V], yb[V];
+    auto rsrc = [&](const T* base, int64_t r) __attribute__((always_inline)) {
+        const int64_t left = r < rows ? (ne - r * RE) * (int64_t)sizeof(T) : 0;
+        return make_rsrc(base + (r < rows ? r * RE : 0),
+                         (uint32_t)(left < RE * (int64_t)sizeof(T) ? left : RE * (int64_t)sizeof(T)));
+    };
+    auto load = [&](int64_t r, vec (&pa)[V], vec (&pb)[V]) __attribute__((always_inline)) {
+        const __amdgpu_buffer_rsrc_t ra = rsrc(a, r), rb = rsrc(b, r);
+#pragma unroll
+        for (int k = 0; k < V; ++k) {
+            const uint32_t off = (uint32_t)(k * THREADS + tid) * VB;
+            pa[k] = load_buf<T, VW, 2>(ra, off, 0);
+            pb[k] = load_buf<T, VW, 2>(rb, off, 0);
+        }
+    };
+    auto store = [&](int64_t r, vec (&pa)[V], vec (&pb)[V]) __attribute__((always_inline)) {
+        const __amdgpu_buffer_rsrc_t rc = rsrc(c, r);
+#pragma unroll
+        for (int k = 0; k < V; ++k)
+            store_buf<T, VW, 2>(pa[k] + pb[k], rc, (uint32_t)(k * THREADS + tid) * VB);
+    };
+    const int64_t step = gridDim.x;
+    int64_t r = blockIdx.x;
+    if (r < rows)
+        load(r, xa, xb);
+    while (r < rows) {
+        load(r + step, ya, yb);
+        store(r, xa, xb);
+        r += step;
+        if (r >= rows)
+            break;
+        load(r + step, xa, xb);
+        store(r, ya, yb);
+        r += step;
+    }
+    if (blockIdx.x == 0 && (int64_t)tid < n - ne) {
+        const int64_t k = ne + tid;
+        c[k] = a[k] + b[k];
+    }
+}
+
 }  // namespace mep

@@ -98,10 +98,11 @@ def test_workspace_sizes():
     assert mep.mep_workspace_bytes(mep.MEP_OP_REDUCE_SUM, f32, 1, 0) == 0
     assert mep.mep_workspace_bytes(mep.MEP_OP_VECTOR_ADD, f64, 1, 1000) == 0
     assert mep.mep_variant_count(mep.MEP_OP_REDUCE_SUM, f32, 1, 1000) == 1
-    assert mep.mep_variant_count(mep.MEP_OP_VECTOR_ADD, f32, 1, 1000) == 4
-    assert "rows" in mep.mep_variant_info(mep.MEP_OP_VECTOR_ADD, f32, 1, 1000, 2)
+    assert mep.mep_variant_count(mep.MEP_OP_VECTOR_ADD, f32, 1, 1000) == 6
+    assert "chunks" in mep.mep_variant_info(mep.MEP_OP_VECTOR_ADD, f32, 1, 1000, 2)
+    assert "buffer rows" in mep.mep_variant_info(mep.MEP_OP_VECTOR_ADD, f32, 1, 1000, 0)
     with pytest.raises(mep.MepError):
-        mep.mep_variant_info(mep.MEP_OP_VECTOR_ADD, f32, 1, 1000, 4)
+        mep.mep_variant_info(mep.MEP_OP_VECTOR_ADD, f32, 1, 1000, 6)
     # GEMVER: pass 1 column partials or pass 2 dot partials, whichever is larger
     assert ws(mep.MEP_OP_GEMVER, f32, 16384, 16384) >= 64 * 16384 * 4
     assert ws(mep.MEP_OP_GEMVER, f64, 0, 100) == 0
