@@ -89,7 +89,7 @@ def parse():
     ap.add_argument("--probe-copy", action="store_true",
                     help="also run the 1 GiB streaming-copy probe (counter calibration)")
     ap.add_argument("--no-ceiling", action="store_true",
-                    help="skip the HBM ceiling probe (a 2 GiB read-sum)")
+                    help="skip the HBM ceiling probe (a read-sum of as many bytes as the workload streams)")
     ap.add_argument("--variant", type=int, default=-1, help="kernel candidate (Eqs. 4-5); -1 default")
     ap.add_argument("--select", action="store_true",
                     help="also run one round of candidate selection (Eqs. 3-5, cold cache) and report "
@@ -479,13 +479,27 @@ def probe_read(n: int, dtype: str = "f32", reps: int = 20) -> float:
     return n * es / (tot / cnt * 1e-3) / 1e9
 
 
-def probe_ceiling():
-    """HBM read ceiling: the library's sum over ~2 GiB of fp32 (a pure stream;
-    the longest vector the library accepts, 65535 x 8192 elements)."""
-    n = 65535 * 8192
+def stream_read_bytes(w, dtype: str) -> int:
+    """Bytes the workload's dominant kernel streams from memory: the matrix
+    (both for GESUMMV), the vector for the sum, both inputs for the add."""
+    es = 4 if dtype == "f32" else 8
+    if w.op == "reduce_sum":
+        return w.n * es
+    if w.op == "vector_add":
+        return 2 * w.n * es
+    return (2 if w.op == "axpby_mv" else 1) * w.m * w.n * es
+
+
+def probe_ceiling(nbytes: int):
+    """HBM read ceiling: the library's sum (a pure stream) over as many bytes
+    as the workload's dominant kernel reads, so that the kernel is compared
+    with a read of its own size (a 2 GiB stream reads a few % slower than a
+    1 GiB one); at most the longest vector the library accepts, 65535 x 8192
+    fp32 elements."""
+    n = max(1, min(nbytes // 4, 65535 * 8192))
     gbs = probe_read(n)
     log(f"[bench] HBM ceiling probe: sum of {n * 4} B fp32, {gbs:.1f} GB/s")
-    return {"kernel": "k_reduce_sum (fp32, 65535 x 8192 elements)", "bytes_read": n * 4, "gbs": round(gbs, 1),
+    return {"kernel": f"k_reduce_sum (fp32, {n} elements)", "bytes_read": n * 4, "gbs": round(gbs, 1),
             "frac_of_peak": round(gbs / PEAK_GBS, 4)}
 
 
@@ -594,7 +608,8 @@ def main():
         print(f"unknown workload {args.workload}; known: {sorted(datagen.WORKLOADS)}", file=sys.stderr)
         sys.exit(2)
     # the ceiling first: HBM throughput read right after minutes of streaming is a few % lower
-    ceiling = None if args.no_ceiling else probe_ceiling()
+    ceiling = None if args.no_ceiling else probe_ceiling(
+        stream_read_bytes(datagen.WORKLOADS[args.workload], args.dtype))
     t_mep = time.perf_counter()
     prim = run_gpu(args.workload, args.dtype, args.steps, args.warmup, args.variant, not args.no_eq3)
     # the MEP proper: input generation, upload, warm-up and timed steps
