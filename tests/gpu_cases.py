@@ -155,7 +155,9 @@ def assert_parity(op, got, ref, dt, what="", scales=None, dims=None):
     """Normwise error <= TOL is the pass criterion; the element-wise and
     condition-scaled errors are printed beside it, and with `scales` (from
     condition_scales) and `dims` = (m, n) the condition-scaled error must also
-    stay within cond_bound."""
+    stay within cond_bound -- a per-element check that bites on outputs whose
+    own scale is far below max|ref| (with inputs of one magnitude it is the
+    looser of the two)."""
     tol = TOL[dt]
     for k, r in ref.items():
         assert got[k].shape == r.shape, f"{what} {k}: shape {got[k].shape} vs {r.shape}"
