@@ -642,13 +642,12 @@ static int run_matvec_t(int64_t m, int64_t n, const T* A, const T* w, T* z, cons
     return e == hipSuccess ? MEP_OK : hip_fail(e, "matvec_t launch");
 }
 
-// Workspace bytes the ATAX call with these operands really uses (the plan
-// of the op's current variant; mep_workspace_bytes covers every candidate).
-static size_t ata_x_used_bytes(int esize, bool vec, int64_t m, int64_t n)
+// Workspace bytes the ATAX call with these operands really uses under the
+// given variant (mep_workspace_bytes covers every candidate).
+static size_t ata_x_used_bytes(int esize, bool vec, int64_t m, int64_t n, int variant)
 {
     if (m == 0 || n == 0)
         return 0;
-    const int variant = g_variant[MEP_OP_ATA_X].load(std::memory_order_relaxed);
     const Plan p = plan_stream(esize, vec, MODE_ATAX, m, n, variant);
     if (p.panels == 1)
         return layout_for(MODE_ATAX, p, esize, m, n, false).total;
@@ -659,7 +658,8 @@ static size_t ata_x_used_bytes(int esize, bool vec, int64_t m, int64_t n)
 }
 
 template <typename T>
-static int run_ata_x(int64_t m, int64_t n, const T* A, const T* x, T* y, T* t, char* ws, hipStream_t s)
+static int run_ata_x(int64_t m, int64_t n, const T* A, const T* x, T* y, T* t, char* ws, hipStream_t s,
+                     int variant)
 {
     hipError_t e = hipSuccess;
     if (n == 0) {
@@ -672,7 +672,7 @@ static int run_ata_x(int64_t m, int64_t n, const T* A, const T* x, T* y, T* t, c
         return e == hipSuccess ? MEP_OK : hip_fail(e, "fill");
     }
     const bool vec = vec_ok_n(sizeof(T), n) && aligned(A, 16) && aligned(x, 16);
-    const Plan p = plan_stream(sizeof(T), vec, MODE_ATAX, m, n, variant_of(MEP_OP_ATA_X));
+    const Plan p = plan_stream(sizeof(T), vec, MODE_ATAX, m, n, variant);
     if (p.panels == 1) {
         // one pass: row dot, then the same row scaled by it into the column sums
         StreamArgs<T> a = empty_args<T>(m, n);
@@ -686,8 +686,8 @@ static int run_ata_x(int64_t m, int64_t n, const T* A, const T* x, T* y, T* t, c
         return e == hipSuccess ? MEP_OK : hip_fail(e, "ata_x launch");
     }
     // rows too long to keep on chip: t = A x over column panels, then A^T t
-    const Plan p1 = plan_stream(sizeof(T), vec, MODE_MV, m, n, variant_of(MEP_OP_ATA_X));
-    const Plan p2 = plan_stream(sizeof(T), vec, MODE_ATW, m, n, variant_of(MEP_OP_ATA_X));
+    const Plan p1 = plan_stream(sizeof(T), vec, MODE_MV, m, n, variant);
+    const Plan p2 = plan_stream(sizeof(T), vec, MODE_ATW, m, n, variant);
     const WsLayout l1 = layout_for(MODE_MV, p1, sizeof(T), m, n, true);
     T* dot = reinterpret_cast<T*>(ws);
     T* tt = t != nullptr ? t : reinterpret_cast<T*>(ws + l1.dotpart);
@@ -1041,9 +1041,12 @@ int mep_ata_x(int dtype, int64_t m, int64_t n, const void* A, const void* x, voi
     if ((rc = check_overlaps(outs, 2, ins, 3)))
         return rc;
     hipStream_t s = (hipStream_t)stream;
+    const int variant = variant_of(MEP_OP_ATA_X);
     if (dtype == MEP_F32)
-        return run_ata_x<float>(m, n, (const float*)A, (const float*)x, (float*)y, (float*)t, (char*)ws, s);
-    return run_ata_x<double>(m, n, (const double*)A, (const double*)x, (double*)y, (double*)t, (char*)ws, s);
+        return run_ata_x<float>(m, n, (const float*)A, (const float*)x, (float*)y, (float*)t, (char*)ws, s,
+                                variant);
+    return run_ata_x<double>(m, n, (const double*)A, (const double*)x, (double*)y, (double*)t, (char*)ws, s,
+                             variant);
 }
 
 }  // extern "C"
@@ -1109,8 +1112,11 @@ int mep_ata_x_noalloc(int dtype, int64_t m, int64_t n, const void* A, const void
         return rc;
     if (t != nullptr && (rc = check_ptr(t, m, es, "t")))
         return rc;
+    // one reading of the op's variant sizes the call and plans it, so a
+    // concurrent mep_set_variant cannot make the plan outgrow the scratch
+    const int variant = variant_of(MEP_OP_ATA_X);
     const bool vec = vec_ok_n(es, n) && aligned(A, 16) && aligned(x, 16);
-    const size_t need = ata_x_used_bytes(es, vec, m, n);
+    const size_t need = ata_x_used_bytes(es, vec, m, n, variant);
     if (need > kNoAllocScratchBytes)
         return fail(MEP_EWORKSPACE, "this call needs %zu bytes of scratch; the allocation-free entry point "
                     "holds %zu (use mep_ata_x with a workspace)", need, kNoAllocScratchBytes);
@@ -1127,8 +1133,10 @@ int mep_ata_x_noalloc(int dtype, int64_t m, int64_t n, const void* A, const void
     if ((rc = scratch_on(dev, &ws)))
         return rc;
     if (dtype == MEP_F32)
-        return run_ata_x<float>(m, n, (const float*)A, (const float*)x, (float*)y, (float*)t, (char*)ws, s);
-    return run_ata_x<double>(m, n, (const double*)A, (const double*)x, (double*)y, (double*)t, (char*)ws, s);
+        return run_ata_x<float>(m, n, (const float*)A, (const float*)x, (float*)y, (float*)t, (char*)ws, s,
+                                variant);
+    return run_ata_x<double>(m, n, (const double*)A, (const double*)x, (double*)y, (double*)t, (char*)ws, s,
+                             variant);
 }
 
 int mep_axpby_mv(int dtype, int64_t m, int64_t n, double alpha, const void* A, double beta, const void* B,
