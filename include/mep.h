@@ -119,7 +119,8 @@ int mep_ata_x(int dtype, int64_t m, int64_t n, const void* A, const void* x, voi
  * that the library owns on each GPU: MEP_NOALLOC_SCRATCH_BYTES (64 MiB),
  * reserved on a device when the library's code is first loaded there and
  * held until the process ends; its address is looked up on the first call on
- * a device.  The call allocates and frees nothing.  A call whose plan needs
+ * a device, which must therefore be made outside a graph capture (later calls
+ * may be captured and replayed).  The call allocates and frees nothing.  A call whose plan needs
  * more scratch than that (e.g. a row too long to keep on chip, which takes
  * the two-pass path over a huge m) returns MEP_EWORKSPACE and launches
  * nothing.  Every call on one GPU shares that GPU's scratch: calls that may

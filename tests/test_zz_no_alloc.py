@@ -81,3 +81,40 @@ def test_noalloc_refuses_a_plan_beyond_its_scratch():
                              ctypes.c_void_p((1 << 40) + (1 << 43)), None, None)
     assert rc == mep.MEP_EWORKSPACE
     assert "64" in mep.mep_last_error() or str(mep.NOALLOC_SCRATCH_BYTES) in mep.mep_last_error()
+
+
+@pytest.mark.parametrize("dt", [np.float32, np.float64], ids=["f32", "f64"])
+def test_noalloc_replays_from_a_captured_graph(dt):
+    """The callers it is for include code under graph capture: the call is
+    captured on a side stream (after one eager call, which looks up the
+    scratch address) and replayed four times, with eager work and
+    synchronizations between the replays; every replay equals the eager
+    result bit for bit."""
+    import torch
+
+    dev = torch.device("cuda:0")
+    tdt = torch.float32 if dt == np.float32 else torch.float64
+    m, n = 3000, 4100
+    print(f"noalloc graph {np.dtype(dt).name}: {m}x{n}", flush=True)
+    A = torch.from_numpy(datagen.uniform(50, 0, (m, n), dt)).to(dev)
+    x = torch.from_numpy(datagen.uniform(50, 1, (n,), dt)).to(dev)
+    y = torch.empty(n, dtype=tdt, device=dev)
+    t = torch.empty(m, dtype=tdt, device=dev)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        assert _raw_noalloc(dt, A, x, y, t) == mep.MEP_OK, mep.mep_last_error()
+    torch.cuda.synchronize()
+    y_eager, t_eager = y.clone(), t.clone()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=s):
+        rc = _raw_noalloc(dt, A, x, y, t)
+    assert rc == mep.MEP_OK, mep.mep_last_error()
+    for rep in range(4):
+        junk = torch.randn(1 << 20, device=dev).sum()
+        torch.cuda.synchronize()
+        y.fill_(float("nan"))
+        t.fill_(float("nan"))
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y, y_eager) and torch.equal(t, t_eager), f"replay {rep} differs from the eager call"
+        del junk
