@@ -294,7 +294,10 @@ int mep_variant_info(int op, int dtype, int64_t m, int64_t n, int variant, char*
  * after Eq. 5), each round generating new candidates.  Here the candidate set
  * is fixed, so a second round would only re-find the same argmin: one round
  * is the whole search, and the call takes neither D nor a threshold.
- * Synchronizes call->stream; overwrites the call's outputs.
+ * Synchronizes call->stream; overwrites the call's outputs.  While it runs,
+ * the op's process-wide variant steps through the candidates: a call of the
+ * same op from another host thread meanwhile runs whichever candidate is set
+ * (each one correct; only its speed differs).
  */
 typedef struct {
     double mean_ms;
