@@ -267,6 +267,31 @@ def test_argument_errors(L):
     assert rc == mep.MEP_EINVAL and "overlap" in msg
 
 
+MAX_M = 1 << 30
+MAX_N = 65535 * 8192
+
+
+@pytest.mark.parametrize("which", ["m", "n"])
+def test_size_limits_are_exact(L, which):
+    """The largest accepted sizes (m = 2^30 rows, rows of 65535 * 8192
+    elements) pass the size check and one more fails it.  A is given one
+    byte off its element alignment, so an accepted size stops at the next
+    check (MEP_EALIGN) and nothing is ever launched."""
+    bad_a = FAKE + 1
+    for dt in (mep.MEP_F32, mep.MEP_F64):
+        for size, want in ((MAX_M if which == "m" else MAX_N, mep.MEP_EALIGN),
+                           ((MAX_M if which == "m" else MAX_N) + 1, mep.MEP_EINVAL)):
+            m, n = (size, 1) if which == "m" else (1, size)
+            rc, msg = _rc(L.mep_matvec, dt, m, n, bad_a, FAKE, FAKE, None, 0, None)
+            assert rc == want, (dt, m, n, msg)
+            rc, msg = _rc(L.mep_ata_x, dt, m, n, bad_a, FAKE, FAKE, None, None, 0, None)
+            assert rc == want, (dt, m, n, msg)
+            rc, msg = _rc(L.mep_ata_x_noalloc, dt, m, n, bad_a, FAKE, FAKE, None, None)
+            assert rc == want, (dt, m, n, msg)
+            if want == mep.MEP_EINVAL:
+                assert "2^30" in msg or "row length" in msg, msg
+
+
 def test_harness_errors(L):
     c = mep.MepCall()
     c.op, c.dtype, c.m, c.n = mep.MEP_OP_ATA_X, mep.MEP_F32, 8, 8
