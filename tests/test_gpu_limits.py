@@ -7,6 +7,7 @@
   outputs (A^T w, BICG's s, ATAX's y, GEMVER's x) are wider than one launch
   of the column reduce covers.
 - 2^30 rows of one element, the most rows accepted (4 GiB fp32).
+- The sum and the element-wise add over the longest accepted vector.
 
 Every op runs on each; inputs come from the seeded generator, and every
 output is compared in full with the oracle's by the normwise metric, in
@@ -15,6 +16,7 @@ slices so that no fp64 temporary of a whole output is formed.
 import numpy as np
 import pytest
 
+import oracle
 from tests.gpu_cases import OPS, TOL, gpu_outputs, make_inputs, oracle_outputs
 
 pytestmark = pytest.mark.gpu
@@ -68,3 +70,45 @@ def test_largest_accepted_sizes(dts, m, n, op):
         err = normwise_sliced(got[k], r)
         print(f"limits {op} {dts} {m}x{n} {k}: normwise {err:.3e}", flush=True)
         assert err <= TOL[dt], f"{op} {dts} {m}x{n} {k}: normwise error {err:.3e} > {TOL[dt]:.0e}"
+
+
+VECTOR_CASES = [("f32", MAX_N - 1), ("f64", MAX_N)]
+
+
+@pytest.mark.parametrize("dts,n", VECTOR_CASES, ids=[f"{d}-{n}" for d, n in VECTOR_CASES])
+def test_vector_samples_at_the_longest_length(dts, n):
+    """The sum (non-negative terms, held to the summation-depth bound and the
+    product tolerance) and the element-wise add (bit-exact, every candidate)
+    over the longest accepted vector; the fp32 length leaves a ragged tail
+    after the last 16-byte vector."""
+    import torch
+
+    from paper_2512_22147_amd import datagen, mep
+    from tests.sum_bound import sum_error_bound
+
+    dt = np.float32 if dts == "f32" else np.float64
+    print(f"limits vector samples {dts} n={n}: drawing inputs", flush=True)
+    a = datagen.uniform(33, 0, (n,), dt)
+    np.abs(a, out=a)
+    ad = torch.from_numpy(a).to("cuda:0")
+    got = float(mep.mep_reduce_sum(ad).cpu()[0])
+    ref = oracle.reduce_sum(a)
+    err = abs(got - ref) / abs(ref)
+    print(f"limits reduce_sum {dts} n={n}: relative error {err:.3e}", flush=True)
+    assert err <= min(TOL[dt], sum_error_bound(n, dt)), err
+    b = datagen.normal(33, 1, (n,), dt)
+    bd = torch.from_numpy(b).to("cuda:0")
+    want = oracle.vector_add(a, b).astype(dt)
+    del b
+    code = mep.MEP_F32 if dt == np.float32 else mep.MEP_F64
+    try:
+        for v in range(mep.mep_variant_count(mep.MEP_OP_VECTOR_ADD, code, 1, n)):
+            mep.mep_set_variant(mep.MEP_OP_VECTOR_ADD, v)
+            c = mep.mep_vector_add(ad, bd)
+            torch.cuda.synchronize()
+            same = np.array_equal(c.cpu().numpy(), want)
+            print(f"limits vector_add {dts} n={n} candidate {v}: bit-exact {same}", flush=True)
+            assert same, f"candidate {v}"
+            del c
+    finally:
+        mep.mep_set_variant(mep.MEP_OP_VECTOR_ADD, -1)
