@@ -115,7 +115,7 @@ OPS = {
     "axpby_mv": ("MEP_OP_AXPBY_MV", "k_stream (AXPBY mode)", "y = alpha A x + beta B x"),
     "matvec_t": ("MEP_OP_MATVEC_T", "k_stream (A^T w mode)", "z = A^T w"),
     "reduce_sum": ("MEP_OP_REDUCE_SUM", "k_reduce_sum", "s = sum x"),
-    "vector_add": ("MEP_OP_VECTOR_ADD", "k_vector_add", "c = a + b"),
+    "vector_add": ("MEP_OP_VECTOR_ADD", "k_vector_add_buf", "c = a + b"),
     "gemver": ("MEP_OP_GEMVER", "k_stream (GEMVER pass 1: Ahat stored, Ahat^T y)",
                "GEMVER Ahat = A + u1 v1^T + u2 v2^T, x = beta Ahat^T y + z, w = alpha Ahat x"),
 }
