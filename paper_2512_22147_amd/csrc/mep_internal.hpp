@@ -15,7 +15,8 @@ namespace mep {
 // register budget is 512 / WPE per lane), AUX the cache-policy bits of the
 // matrix loads (0 = default, 2 = non-temporal streaming).  MAP and CUX are
 // launch arguments, not part of the instance: MAP hands row blocks to
-// workgroups cyclically (0) or in contiguous runs (1); CUX is how many of
+// workgroups cyclically (0), in contiguous runs (1) or cyclically with the
+// positions rotated from one window of blocks to the next (2); CUX is how many of
 // each XCD's 32 compute units the grid is sized for (workgroups are dealt to
 // the 8 XCDs in turn).  Measured on MI355X, streaming one large matrix from
 // 22-26 compute units per XCD beats all 32 (fewer rows in flight at once);
@@ -30,7 +31,7 @@ constexpr int kCusPerXcd = 32;
 // Vector path (16-byte loads), ordered by row capacity G * V; among equal
 // capacities the preferred shape comes first (measured on MI355X: streaming
 // the matrix with non-temporal loads is faster for every shape).
-constexpr int kNumVecCfg = 53;
+constexpr int kNumVecCfg = 54;
 constexpr Cfg kVecCfg[kNumVecCfg] = {
     // rows of 1-8 vectors: 2, 4 or 8 lanes per row, 32, 16 or 8 rows per wave
     {2, 1, 8, 4, 2},     {2, 1, 8, 4, 0},
@@ -50,7 +51,7 @@ constexpr Cfg kVecCfg[kNumVecCfg] = {
     {1024, 2, 4, 4, 2},  {1024, 2, 4, 4, 0},  {512, 4, 4, 2, 2},   {512, 4, 4, 2, 0},
     {512, 4, 4, 2, 2, 0, 24},
     // 4096 vectors: a 16384-element fp32 row
-    {512, 8, 2, 2, 2, 0, 24}, {512, 8, 2, 2, 2, 0, 22}, {512, 8, 2, 2, 2}, {512, 8, 2, 2, 2, 1},
+    {512, 8, 2, 2, 2, 2, 24}, {512, 8, 2, 2, 2, 0, 24}, {512, 8, 2, 2, 2, 0, 22}, {512, 8, 2, 2, 2}, {512, 8, 2, 2, 2, 1},
     {1024, 4, 2, 4, 2},  {1024, 4, 2, 4, 2, 0, 24}, {512, 8, 1, 4, 2}, {256, 16, 1, 2, 2},
     {512, 8, 2, 2, 0},   {1024, 4, 2, 4, 0},   {512, 8, 1, 4, 0},   {256, 16, 1, 2, 0},
     // 8192 vectors: a 16384-element fp64 row or a 32768-element fp32 row

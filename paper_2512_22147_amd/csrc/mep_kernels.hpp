@@ -66,7 +66,7 @@ struct StreamArgs {
     T* Aout;           // the updated matrix (may equal A)
     T alpha, beta;
     int64_t m, n, ldp;
-    int blocked;       // row blocks: 0 = block k to workgroup k mod gridDim.x, 1 = contiguous runs
+    int blocked;       // row-block map: 0 cyclic, 1 contiguous runs, 2 rotated cyclic (see k_stream)
     int scale_rows;    // MV: rowout = alpha * dot instead of dot
 };
 
@@ -79,6 +79,10 @@ constexpr int kWriteThrough = 17;
 constexpr int kRsrcWord3 = 0x00020000;
 // A lane offset that is past the end of every resource built here.
 constexpr uint32_t kOutOfRange = 0x40000000u;
+// Shift per round of the rotated row-block map, in blocks (odd, so that the
+// position of a workgroup's blocks in each window, and its address bits,
+// cycle through every residue).
+constexpr int kRotStride = 25;
 
 // Buffer resource for `bytes` bytes at `base`.  Both must be wave-uniform;
 // the size is pinned to a scalar register so that the descriptor never ends
@@ -527,32 +531,48 @@ k_stream(StreamArgs<T> a)
         (void)parity;
     };
 
-    // Row blocks blockIdx.x, blockIdx.x + gridDim.x, ...; the trip count is
-    // uniform across the workgroup, so the barriers inside are too.
-    // Row blocks of this workgroup: blockIdx.x, blockIdx.x + gridDim.x, ...
-    // (cyclic) or one contiguous run (blocked).  The trip count is uniform
-    // across the workgroup, so the barriers inside are too.  The next block
-    // is always prefetched: past the workgroup's last row its resources are
-    // empty, so those loads return zeros without touching memory.  The
-    // scheduling fences keep each refill after the previous use of its
+    // Row blocks of this workgroup, one per round r (nbx = gridDim.x):
+    // - cyclic (map 0): block blockIdx.x + r * nbx;
+    // - blocked (map 1): one contiguous run of blocks;
+    // - rotated (map 2): round r covers the same window of nbx blocks as the
+    //   cyclic map, dealt to the workgroups shifted by r * kRotStride, so that
+    //   no workgroup, and no XCD, reads the same position of every window; in
+    //   the last round some workgroups may get a block past the matrix.
+    // The round count is uniform across the workgroup, so the barriers inside
+    // are too.  The next block is always prefetched: past the last row of the
+    // matrix (or of a blocked run) its resources are empty, so those loads
+    // return zeros without touching memory, and such a block adds nothing.
+    // The scheduling fences keep each refill after the previous use of its
     // buffer, so no more than two batches are ever live.
     const int nblk = (int)((m + BR - 1) / BR);
-    int blk, bstep, bend;
-    if (a.blocked) {
+    const int map = a.blocked;
+    int blk0, bstep, bend;
+    if (map == 1) {
         const int per = (nblk + nbx - 1) / nbx;
-        blk = blockIdx.x * per;
+        blk0 = blockIdx.x * per;
         bstep = 1;
-        bend = blk + per < nblk ? blk + per : nblk;
+        bend = blk0 + per < nblk ? blk0 + per : nblk;
     } else {
-        blk = blockIdx.x;
+        blk0 = blockIdx.x;
         bstep = nbx;
         bend = nblk;
     }
-    row_end = bend * BR < m32 ? bend * BR : m32;
+    const int rounds =
+        map == 2 ? (nblk + nbx - 1) / nbx : (blk0 < bend ? (bend - blk0 + bstep - 1) / bstep : 0);
+    row_end = map == 2 ? m32 : (bend * BR < m32 ? bend * BR : m32);
+    auto block_of = [&](int r) __attribute__((always_inline)) -> int {
+        if (map == 2) {
+            const unsigned un = (unsigned)nbx;
+            const int shift = (int)(((unsigned)r % un) * ((unsigned)kRotStride % un) % un);
+            const int pos = (int)blockIdx.x + shift;
+            return r * nbx + (pos < nbx ? pos : pos - nbx);
+        }
+        return blk0 + r * bstep;
+    };
     // the first batch goes out before the column vectors: those come from L2
     // (every workgroup reads the same slice), the matrix from HBM
-    if (blk < bend)
-        load_batch(blk, ra, sa, wa, ua);
+    if (rounds > 0)
+        load_batch(block_of(0), ra, sa, wa, ua);
     if constexpr (NXV > 0) {
 #pragma unroll
         for (int k = 0; k < NXV; ++k) {
@@ -570,21 +590,20 @@ k_stream(StreamArgs<T> a)
         }
     }
 
-    if (blk < bend) {
+    if (rounds > 0) {
+        int r = 0;
         for (;;) {
-            load_batch(blk + bstep, rb, sb, wb, ub);
+            load_batch(block_of(r + 1), rb, sb, wb, ub);
             __builtin_amdgcn_sched_barrier(0);
-            process(blk, 0, ra, sa, wa, ua);
+            process(block_of(r), 0, ra, sa, wa, ua);
             __builtin_amdgcn_sched_barrier(0);
-            blk += bstep;
-            if (blk >= bend)
+            if (++r >= rounds)
                 break;
-            load_batch(blk + bstep, ra, sa, wa, ua);
+            load_batch(block_of(r + 1), ra, sa, wa, ua);
             __builtin_amdgcn_sched_barrier(0);
-            process(blk, 1, rb, sb, wb, ub);
+            process(block_of(r), 1, rb, sb, wb, ub);
             __builtin_amdgcn_sched_barrier(0);
-            blk += bstep;
-            if (blk >= bend)
+            if (++r >= rounds)
                 break;
         }
     }

@@ -527,3 +527,38 @@ def test_small_rows_and_columns(op, dt):
         mep.mep_set_variant(code, v)
         got = gpu_outputs(op, ins, dt)
         assert_parity(op, got, ref, dt, what=f"{m}x{n} candidate {v}", scales=scales, dims=(m, n))
+
+
+ROTATED_SHAPES = [(1, 11300), (385, 12292), (2731, 12300), (5000, 16384)]
+
+
+@pytest.mark.parametrize("op", OPS)
+@pytest.mark.parametrize("shape", ROTATED_SHAPES, ids=lambda s: f"{s[0]}x{s[1]}")
+def test_rotated_block_map(op, shape):
+    """The rotated row-block map (fp32 rows of 2817-4096 vectors): one row,
+    a second round holding a single block, and several rounds with a ragged
+    last one, including a streamed matrix (default shape); the same bits on
+    a second run."""
+    from paper_2512_22147_amd import mep
+
+    m, n = shape
+    dt = np.float32
+    ins = make_inputs(op, m, n, dt, seed=7000 + m)
+    ref = oracle_outputs(op, ins, dt)
+    scales = condition_scales(op, ins, dt)
+    code = op_code(op)
+    infos = [mep.mep_variant_info(code, mep.MEP_F32, m, n, v)
+             for v in range(mep.mep_variant_count(code, mep.MEP_F32, m, n))]
+    rot = [v for v, s in enumerate(infos) if "rotated" in s]
+    assert rot, infos
+    if m * n * 4 > (128 << 20) and op not in ("axpby_mv", "gemver"):
+        assert rot[0] == 0, "a streamed row of this length takes the rotated map by default"
+    try:
+        mep.mep_set_variant(code, rot[0])
+        got = gpu_outputs(op, ins, dt)
+        again = gpu_outputs(op, ins, dt)
+    finally:
+        mep.mep_set_variant(code, -1)
+    assert_parity(op, got, ref, dt, what=f"{m}x{n} {infos[rot[0]]}", scales=scales, dims=(m, n))
+    for k in got:
+        assert got[k].tobytes() == again[k].tobytes(), f"{k} differs between two runs"
