@@ -31,7 +31,7 @@ constexpr int kCusPerXcd = 32;
 // Vector path (16-byte loads), ordered by row capacity G * V; among equal
 // capacities the preferred shape comes first (measured on MI355X: streaming
 // the matrix with non-temporal loads is faster for every shape).
-constexpr int kNumVecCfg = 54;
+constexpr int kNumVecCfg = 55;
 constexpr Cfg kVecCfg[kNumVecCfg] = {
     // rows of 1-8 vectors: 2, 4 or 8 lanes per row, 32, 16 or 8 rows per wave
     {2, 1, 8, 4, 2},     {2, 1, 8, 4, 0},
@@ -55,7 +55,7 @@ constexpr Cfg kVecCfg[kNumVecCfg] = {
     {1024, 4, 2, 4, 2},  {1024, 4, 2, 4, 2, 0, 24}, {512, 8, 1, 4, 2}, {256, 16, 1, 2, 2},
     {512, 8, 2, 2, 0},   {1024, 4, 2, 4, 0},   {512, 8, 1, 4, 0},   {256, 16, 1, 2, 0},
     // 8192 vectors: a 16384-element fp64 row or a 32768-element fp32 row
-    {512, 16, 1, 2, 2, 0, 26}, {512, 16, 1, 2, 2, 0, 24}, {512, 16, 1, 2, 2}, {512, 16, 1, 2, 2, 1},
+    {512, 16, 1, 2, 2, 2, 26}, {512, 16, 1, 2, 2, 0, 26}, {512, 16, 1, 2, 2, 0, 24}, {512, 16, 1, 2, 2}, {512, 16, 1, 2, 2, 1},
     {1024, 8, 1, 4, 2},  {256, 32, 1, 1, 2},   {512, 16, 1, 2, 0},  {1024, 8, 1, 4, 0},
     {256, 32, 1, 1, 0}};
 // Element-wise path (rows not 16-byte aligned): one element per load, so

@@ -319,6 +319,23 @@ k_stream(StreamArgs<T> a)
 #pragma unroll
     for (int v = 0; v < (COL ? V : 1); ++v)
         acc[v] = zero;
+    // Where a lane's row buffers and column sums leave no room for the rest
+    // (16 vectors per lane at 2 waves per SIMD), the compiler spilled a few
+    // registers to scratch, and each reload waited for every load in flight
+    // (the prefetched row included).  The last NACCL column sums of each lane
+    // live in LDS there instead; the counts are the smallest that leave these
+    // instances without spills (fp32 A^T w 4; fp32 BICG and ATAX 3; fp64 ATAX 3).
+    constexpr int NACCL = !(COL && WIDE && RG == 1 && V == 16 && WPE == 2 && !RANK2)
+                              ? 0
+                              : (DOT ? (FROMDOT || ES == 4 ? 3 : 0) : (ES == 4 ? 4 : 0));
+    __shared__ vec accl[NACCL > 0 ? NACCL * THREADS : 1];
+    static_assert(sizeof(xs) + sizeof(red) + sizeof(cred) + sizeof(accl) <= 160 * 1024,
+                  "LDS of one workgroup above the 160 KiB of a compute unit");
+    if constexpr (NACCL > 0) {
+#pragma unroll
+        for (int k = 0; k < NACCL; ++k)
+            accl[k * THREADS + tid] = zero;
+    }
 
     int row_end = m32;  // rows at or past this read as zeros (set before the loop)
     vec ra[B][V], rb[B][V];
@@ -522,10 +539,20 @@ k_stream(StreamArgs<T> a)
                 else
                     s = wbuf[j];
 #pragma unroll
-                for (int v = 0; v < V; ++v)
+                for (int v = 0; v < V - NACCL; ++v)
 #pragma unroll
                     for (int e = 0; e < VW; ++e)
                         acc[v][e] = fma_t(s, buf[j][v][e], acc[v][e]);
+                if constexpr (NACCL > 0) {
+#pragma unroll
+                    for (int k = 0; k < NACCL; ++k) {
+                        vec t = accl[k * THREADS + tid];
+#pragma unroll
+                        for (int e = 0; e < VW; ++e)
+                            t[e] = fma_t(s, buf[j][V - NACCL + k][e], t[e]);
+                        accl[k * THREADS + tid] = t;
+                    }
+                }
             }
         }
         (void)parity;
@@ -610,6 +637,11 @@ k_stream(StreamArgs<T> a)
 
     if constexpr (COL) {
         T* out = a.colpart + (int64_t)blockIdx.x * a.ldp + col0;
+        if constexpr (NACCL > 0) {
+#pragma unroll
+            for (int k = 0; k < NACCL; ++k)
+                acc[V - NACCL + k] = accl[k * THREADS + tid];
+        }
         if constexpr (RG == 1) {
 #pragma unroll
             for (int v = 0; v < V; ++v) {

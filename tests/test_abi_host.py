@@ -124,7 +124,7 @@ def test_workspace_sizes():
 MEASURED_DEFAULTS = [
     # the benchmark workloads
     ("ATA_X", 0, 16384, 16384, "G=512 V=8 B=2 WPE=2 nt rotated cus=24/32"),
-    ("ATA_X", 1, 16384, 16384, "G=512 V=16 B=1 WPE=2 nt cyclic cus=26/32"),
+    ("ATA_X", 1, 16384, 16384, "G=512 V=16 B=1 WPE=2 nt rotated cus=26/32"),
     ("ATA_X", 0, 1024, 1024, "G=64 V=4 B=2 WPE=4 nt"),
     ("BICG", 0, 4096, 4096, "G=512 V=2 B=8 WPE=2 nt cyclic cus=32/32"),
     ("AXPBY_MV", 0, 8192, 8192, "G=512 V=8 B=1 WPE=2 nt cyclic cus=32/32"),
@@ -142,12 +142,14 @@ MEASURED_DEFAULTS = [
     ("AXPBY_MV", 0, 8192, 16384, "G=512 V=8 B=1 WPE=2 nt cyclic cus=24/32"),
     ("GEMVER", 0, 131072, 2048, "G=512 V=2 B=8 WPE=2 nt"),
     ("GEMVER", 1, 131072, 1024, "G=256 V=4 B=2 WPE=4 nt"),
-    # streamed fp32 rows past 2816 vectors: the rotated block map; shorter
-    # rows and fp64 keep the cyclic one
+    # streamed fp32 rows past 2816 vectors, and fp64 ATAX rows past 5632
+    # vectors: the rotated block map; the rest keep the cyclic one
     ("MATVEC_T", 0, 20000, 15000, "G=512 V=8 B=2 WPE=2 nt rotated cus=24/32"),
     ("BICG", 0, 22000, 12200, "G=512 V=8 B=2 WPE=2 nt rotated cus=24/32"),
     ("MATVEC", 0, 27000, 10000, "G=512 V=8 B=2 WPE=2 nt cyclic cus=24/32"),
     ("ATA_X", 1, 16000, 8000, "G=512 V=8 B=2 WPE=2 nt cyclic cus=22/32"),
+    ("ATA_X", 1, 14000, 14000, "G=512 V=16 B=1 WPE=2 nt rotated cus=26/32"),
+    ("BICG", 1, 16384, 16384, "G=512 V=16 B=1 WPE=2 nt cyclic cus=26/32"),
     # narrow rows: as many lanes per row as the row has vectors
     ("MATVEC", 0, 1 << 24, 12, "G=4 V=1 B=8 WPE=4 nt cyclic cus=32/32"),
     ("ATA_X", 1, 1 << 24, 8, "G=4 V=1 B=8 WPE=4 nt"),
@@ -160,7 +162,7 @@ MEASURED_DEFAULTS = [
     ("ATA_X", 0, 21838, 12292, "G=512 V=8 B=2 WPE=2 nt rotated cus=24/32"),
     ("MATVEC_T", 0, 13107, 20480, "G=512 V=16 B=1 WPE=2 nt cyclic cus=26/32"),
     ("BICG", 0, 13107, 20480, "G=512 V=16 B=1 WPE=2 nt cyclic cus=32/32"),
-    ("ATA_X", 1, 10922, 12288, "G=512 V=16 B=1 WPE=2 nt cyclic cus=26/32"),
+    ("ATA_X", 1, 10922, 12288, "G=512 V=16 B=1 WPE=2 nt rotated cus=26/32"),
     ("MATVEC", 0, 1024, 20480, "G=1024 V=8 B=1 WPE=4 nt"),
     # cache-resident
     ("MATVEC", 0, 4096, 2048, "G=256 V=2 B=4 WPE=4 nt"),

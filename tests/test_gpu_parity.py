@@ -529,30 +529,35 @@ def test_small_rows_and_columns(op, dt):
         assert_parity(op, got, ref, dt, what=f"{m}x{n} candidate {v}", scales=scales, dims=(m, n))
 
 
-ROTATED_SHAPES = [(1, 11300), (385, 12292), (2731, 12300), (5000, 16384)]
+ROTATED_CASES = [(np.float32, 1, 11300), (np.float32, 385, 12292), (np.float32, 2731, 12300),
+                 (np.float32, 5000, 16384), (np.float64, 1, 12000), (np.float64, 211, 12300),
+                 (np.float64, 1500, 12300), (np.float64, 3000, 16384)]
 
 
 @pytest.mark.parametrize("op", OPS)
-@pytest.mark.parametrize("shape", ROTATED_SHAPES, ids=lambda s: f"{s[0]}x{s[1]}")
-def test_rotated_block_map(op, shape):
-    """The rotated row-block map (fp32 rows of 2817-4096 vectors): one row,
-    a second round holding a single block, and several rounds with a ragged
-    last one, including a streamed matrix (default shape); the same bits on
-    a second run."""
+@pytest.mark.parametrize("case", ROTATED_CASES,
+                         ids=lambda c: f"{'f32' if c[0] == np.float32 else 'f64'}-{c[1]}x{c[2]}")
+def test_rotated_block_map(op, case):
+    """The rotated row-block map (fp32 rows of 2817-4096 vectors, fp64 rows
+    of 5633-8192): one row, a second round holding a single block, and
+    several rounds with a ragged last one, including streamed matrices (the
+    default shape for fp32 y = A x, A^T w, BICG and ATAX, and for fp64
+    ATAX); the same bits on a second run."""
     from paper_2512_22147_amd import mep
 
-    m, n = shape
-    dt = np.float32
+    dt, m, n = case
+    code = op_code(op)
+    dcode = mep.MEP_F32 if dt == np.float32 else mep.MEP_F64
+    infos = [mep.mep_variant_info(code, dcode, m, n, v) for v in range(mep.mep_variant_count(code, dcode, m, n))]
+    rot = [v for v, s in enumerate(infos) if "rotated" in s]
+    if not rot:
+        pytest.skip(f"no rotated candidate for {op} at {m}x{n}")
+    streamed = m * n * np.dtype(dt).itemsize > (128 << 20)
+    if streamed and (op == "ata_x" or (dt == np.float32 and op in ("matvec", "matvec_t", "bicg"))):
+        assert rot[0] == 0, "a streamed row of this length takes the rotated map by default"
     ins = make_inputs(op, m, n, dt, seed=7000 + m)
     ref = oracle_outputs(op, ins, dt)
     scales = condition_scales(op, ins, dt)
-    code = op_code(op)
-    infos = [mep.mep_variant_info(code, mep.MEP_F32, m, n, v)
-             for v in range(mep.mep_variant_count(code, mep.MEP_F32, m, n))]
-    rot = [v for v, s in enumerate(infos) if "rotated" in s]
-    assert rot, infos
-    if m * n * 4 > (128 << 20) and op not in ("axpby_mv", "gemver"):
-        assert rot[0] == 0, "a streamed row of this length takes the rotated map by default"
     try:
         mep.mep_set_variant(code, rot[0])
         got = gpu_outputs(op, ins, dt)
