@@ -320,12 +320,11 @@ k_stream(StreamArgs<T> a)
     for (int v = 0; v < (COL ? V : 1); ++v)
         acc[v] = zero;
     // Where a lane's row buffers and column sums leave no room for the rest
-    // (16 vectors per lane at 2 waves per SIMD), registers would spill to
-    // scratch, and each reload inside the row loop would wait for every load
-    // in flight, the prefetched row included.  The last NACCL column sums of
-    // each lane live in LDS there instead; the counts are the smallest that
-    // leave these instances without spills (fp32 A^T w 4; fp32 BICG and ATAX
-    // 3; fp64 ATAX 3).
+    // (16 vectors per lane at 2 waves per SIMD), the compiler spilled a few
+    // registers to scratch, and each reload waited for every load in flight
+    // (the prefetched row included).  The last NACCL column sums of each lane
+    // live in LDS there instead; the counts are the smallest that leave these
+    // instances without spills (fp32 A^T w 4; fp32 BICG and ATAX 3; fp64 ATAX 3).
     constexpr int NACCL = !(COL && WIDE && RG == 1 && V == 16 && WPE == 2 && !RANK2)
                               ? 0
                               : (DOT ? (FROMDOT || ES == 4 ? 3 : 0) : (ES == 4 ? 4 : 0));
