@@ -81,9 +81,14 @@ static Cfg preferred_shape(int mode, int esize, int64_t m, int64_t n, int64_t nv
     // 5.7-6.6 TB/s for 1 GiB of 12- and 16-element fp32 rows)
     if (nv <= 8) {
         // rows of one vector of a cache-resident matrix: cached loads (3-10%
-        // faster for y = A x, A^T w and BICG)
+        // faster for y = A x, A^T w and BICG).  Otherwise BICG takes 4-row
+        // batches: its 8-row batches spill registers in fp64 (1 GiB of 4- and
+        // 8-vector fp64 rows: 25% faster; fp32 up to 2%)
+        const int g = nv <= 2 ? 2 : (nv <= 4 ? 4 : 8);
+        if (bicg && (nv > 1 || stream))
+            return Cfg{g, 1, 4, 4, 2};
         const int aux1 = nv == 1 && !stream && !atax && !two ? 0 : naux;
-        return Cfg{nv <= 2 ? 2 : (nv <= 4 ? 4 : 8), 1, 8, 4, aux1};
+        return Cfg{g, 1, 8, 4, aux1};
     }
     // rows of <= 16 vectors: 16 compute units per XCD (512 workgroups) halve
     // the partial rows the single-workgroup column reduce adds (the step is

@@ -31,12 +31,13 @@ constexpr int kCusPerXcd = 32;
 // Vector path (16-byte loads), ordered by row capacity G * V; among equal
 // capacities the preferred shape comes first (measured on MI355X: streaming
 // the matrix with non-temporal loads is faster for every shape).
-constexpr int kNumVecCfg = 55;
+constexpr int kNumVecCfg = 58;
 constexpr Cfg kVecCfg[kNumVecCfg] = {
     // rows of 1-8 vectors: 2, 4 or 8 lanes per row, 32, 16 or 8 rows per wave
-    {2, 1, 8, 4, 2},     {2, 1, 8, 4, 0},
-    {4, 1, 8, 4, 2},     {4, 1, 8, 4, 0},
-    {8, 1, 8, 4, 2},     {8, 1, 8, 4, 0},
+    // (4-row batches for BICG, whose 8-row batches spill registers in fp64)
+    {2, 1, 8, 4, 2},     {2, 1, 8, 4, 0},     {2, 1, 4, 4, 2},
+    {4, 1, 8, 4, 2},     {4, 1, 8, 4, 0},     {4, 1, 4, 4, 2},
+    {8, 1, 8, 4, 2},     {8, 1, 8, 4, 0},     {8, 1, 4, 4, 2},
     {16, 1, 8, 4, 2},    {16, 1, 8, 4, 2, 0, 24}, {16, 1, 8, 4, 2, 0, 16}, {16, 1, 8, 4, 0},
     {16, 1, 4, 4, 2},
     {64, 1, 8, 4, 2},    {64, 1, 8, 4, 0},

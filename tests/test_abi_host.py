@@ -154,7 +154,10 @@ MEASURED_DEFAULTS = [
     ("MATVEC", 0, 1 << 24, 12, "G=4 V=1 B=8 WPE=4 nt cyclic cus=32/32"),
     ("ATA_X", 1, 1 << 24, 8, "G=4 V=1 B=8 WPE=4 nt"),
     ("MATVEC_T", 0, 1 << 24, 32, "G=8 V=1 B=8 WPE=4 nt"),
-    ("BICG", 0, 1 << 25, 8, "G=2 V=1 B=8 WPE=4 nt"),
+    ("BICG", 0, 1 << 25, 8, "G=2 V=1 B=4 WPE=4 nt"),
+    ("BICG", 1, 1 << 24, 8, "G=4 V=1 B=4 WPE=4 nt"),
+    ("BICG", 0, 1 << 20, 4, "G=2 V=1 B=8 WPE=4 cached"),
+    ("MATVEC_T", 1, 1 << 24, 8, "G=4 V=1 B=8 WPE=4 nt"),
     ("BICG", 1, 1 << 22, 32, "G=16 V=1 B=4 WPE=4 nt"),
     # rows between the measured lengths: the smallest 512-lane shape that covers them
     ("ATA_X", 0, 65472, 4100, "G=512 V=4 B=4 WPE=2 nt cyclic cus=24/32"),
