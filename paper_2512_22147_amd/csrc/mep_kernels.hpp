@@ -389,6 +389,11 @@ k_stream(StreamArgs<T> a)
                        T (&wbuf)[WTS ? B : 1], T (&ubuf)[RANK2 ? 2 * B : 1])
                        __attribute__((always_inline)) {
         T d[B], d2[TWO ? B : 1];
+        // A row past the end of the matrix reads as zeros, yet its dot (0 * x)
+        // or its rank-2 update (0 * v1 + 0 * v2) is NaN where that vector
+        // holds an infinity, so it must add nothing to the column sums.  Only
+        // a block that reaches past the last row (wave-uniform) has such rows.
+        const bool tail = blk * BR + BR > row_end;
         if constexpr (RANK2) {
             // Ahat_i = A_i + u1_i v1 + u2_i v2, in the registers that hold A_i;
             // each slice of v1 and v2 is read once for the whole batch
@@ -404,6 +409,20 @@ k_stream(StreamArgs<T> a)
                                              fma_t(ubuf[2 * j], v1v[e], buf[j][v][e]));
                 if constexpr (XLDS)
                     __builtin_amdgcn_sched_barrier(0);
+            }
+            if (tail) {
+                // zero the updated rows past the end (the fence keeps these
+                // selects inside the branch, off the path of every other block)
+#pragma unroll
+                for (int j = 0; j < B; ++j) {
+                    const bool in = sub < row_end - (blk * BR + j * RG + wgrp0);
+#pragma unroll
+                    for (int v = 0; v < V; ++v)
+#pragma unroll
+                        for (int e = 0; e < VW; ++e)
+                            buf[j][v][e] = in ? buf[j][v][e] : (T)0;
+                }
+                __builtin_amdgcn_sched_barrier(0);
             }
         }
         if constexpr (STORE) {
@@ -528,6 +547,16 @@ k_stream(StreamArgs<T> a)
                         }
                     }
                 }
+            }
+            if (FROMDOT && tail) {
+                // zero the weight of the rows past the end (fenced into the
+                // branch like the rank-2 rows above)
+#pragma unroll
+                for (int j = 0; j < B; ++j) {
+                    if (sub >= row_end - (blk * BR + j * RG + wgrp0))
+                        d[j] = (T)0;
+                }
+                __builtin_amdgcn_sched_barrier(0);
             }
         }
         if constexpr (COL) {
