@@ -394,6 +394,15 @@ k_stream(StreamArgs<T> a)
         // holds an infinity, so it must add nothing to the column sums.  Only
         // a block that reaches past the last row (wave-uniform) has such rows.
         const bool tail = blk * BR + BR > row_end;
+        // GEMVER's streamed instances with row groups of 512 lanes or more
+        // and batches of up to 4 rows skip such rows in the column sums (one
+        // row per wave: a wave-uniform test).  Besides, that branch keeps the
+        // column sums in their registers: without it the compiler copied them
+        // once per batch, and the first pass ran 3-7% slower on streamed
+        // matrices.  The other instances zero the rows instead: there the
+        // branch cost up to 4% (scalar spills with 8-row batches, shorter rows
+        // and cache-resident matrices).
+        constexpr bool SKIP_PAST = WIDE && RANK2 && G >= 512 && B <= 4 && AUX != 0;
         if constexpr (RANK2) {
             // Ahat_i = A_i + u1_i v1 + u2_i v2, in the registers that hold A_i;
             // each slice of v1 and v2 is read once for the whole batch
@@ -410,7 +419,7 @@ k_stream(StreamArgs<T> a)
                 if constexpr (XLDS)
                     __builtin_amdgcn_sched_barrier(0);
             }
-            if (tail) {
+            if (!SKIP_PAST && tail) {
                 // zero the updated rows past the end (the fence keeps these
                 // selects inside the branch, off the path of every other block)
 #pragma unroll
@@ -562,6 +571,10 @@ k_stream(StreamArgs<T> a)
         if constexpr (COL) {
 #pragma unroll
             for (int j = 0; j < B; ++j) {
+                if constexpr (SKIP_PAST) {
+                    if (blk * BR + j * RG + wgrp0 >= row_end)
+                        continue;
+                }
                 T s;
                 if constexpr (FROMDOT)
                     s = d[j];
