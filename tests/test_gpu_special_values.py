@@ -1,8 +1,9 @@
 """IEEE special values through every operation and every candidate shape.
 
 One NaN or infinity is placed in A (the matrix's last element, or the first
-element of a middle row) or in the vector operand multiplied into A (its last
-element), on shapes that take the row-group path, the element-wise path for
+element of a middle row), in the vector operand multiplied into A (its last
+element), or in another operand (BICG's r, GESUMMV's B, GEMVER's u1, y, z),
+on shapes that take the row-group path, the element-wise path for
 misaligned rows, the narrow-row path and column panels.  With a single
 special value per input and no finite partial sum near overflow, whether an
 output is NaN, +inf, -inf or finite does not depend on the order of
@@ -61,16 +62,12 @@ def _inject(op, ins, where):
         ins[key][(m, n)[axis] - 1] = -np.inf
 
 
-@pytest.mark.parametrize("dt", [np.float32, np.float64], ids=["f32", "f64"])
-@pytest.mark.parametrize("op", OPS)
-@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: f"{s[0]}x{s[1]}")
-@pytest.mark.parametrize("where", ["nan-last-element", "inf-row-start", "neg-inf-vector-last"])
-def test_special_values_every_candidate(where, shape, op, dt):
+def _check_every_candidate(op, ins, dt):
+    """The default and every candidate against the oracle: same class at
+    every output position, finite outputs within the normwise tolerance."""
     from paper_2512_22147_amd import mep
 
-    m, n = shape
-    ins = make_inputs(op, m, n, dt, seed=88 + m + n)
-    _inject(op, ins, where)
+    m, n = ins["A"].shape
     ref = oracle_outputs(op, ins, dt)
     want = {k: _classes(r) for k, r in ref.items()}
     assert any((c != 0).any() for c in want.values()), "the special value reached no output"
@@ -91,3 +88,87 @@ def test_special_values_every_candidate(where, shape, op, dt):
                 err = float(np.max(np.abs(g[fin] - r[fin])))
                 err = err / scale if scale > 0 else err
                 assert err <= TOL[dt], f"{op} {k} candidate {v}: finite outputs differ by {err:.3e}"
+
+
+@pytest.mark.parametrize("dt", [np.float32, np.float64], ids=["f32", "f64"])
+@pytest.mark.parametrize("op", OPS)
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: f"{s[0]}x{s[1]}")
+@pytest.mark.parametrize("where", ["nan-last-element", "inf-row-start", "neg-inf-vector-last"])
+def test_special_values_every_candidate(where, shape, op, dt):
+    m, n = shape
+    ins = make_inputs(op, m, n, dt, seed=88 + m + n)
+    _inject(op, ins, where)
+    _check_every_candidate(op, ins, dt)
+
+
+# the other operands: BICG's r, GESUMMV's B, GEMVER's u1, y and z (operand,
+# position as a function of the shape, value)
+SECOND = [("bicg", "w", lambda m, n: m - 1, np.inf), ("bicg", "w", lambda m, n: 0, np.nan),
+          ("axpby_mv", "B", lambda m, n: (m // 2, 0), np.nan),
+          ("axpby_mv", "B", lambda m, n: (m - 1, n - 1), -np.inf),
+          ("gemver", "u1", lambda m, n: m - 1, np.inf), ("gemver", "y", lambda m, n: m - 1, -np.inf),
+          ("gemver", "z", lambda m, n: n - 1, np.nan)]
+
+
+@pytest.mark.parametrize("dt", [np.float32, np.float64], ids=["f32", "f64"])
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: f"{s[0]}x{s[1]}")
+@pytest.mark.parametrize("case", range(len(SECOND)),
+                         ids=[f"{o}-{k}-{v}" for o, k, _, v in SECOND])
+def test_special_values_in_other_operands(case, shape, dt):
+    op, key, pos, value = SECOND[case]
+    m, n = shape
+    ins = make_inputs(op, m, n, dt, seed=77 + m + n)
+    ins[key][pos(m, n)] = value
+    _check_every_candidate(op, ins, dt)
+
+
+def _sum_class(x):
+    return int(_classes(np.array([x]))[0])
+
+
+@pytest.mark.parametrize("dt", [np.float32, np.float64], ids=["f32", "f64"])
+@pytest.mark.parametrize("n", [5, 4099, (1 << 20) + 3])
+@pytest.mark.parametrize("offset", [0, 1], ids=["aligned", "offset"])
+@pytest.mark.parametrize("case", ["inf", "inf-and-neg-inf", "nan"])
+def test_vector_samples_special_values(case, offset, n, dt):
+    """The sum is +inf (one infinity) or NaN (infinities of both signs, or a NaN)
+    in any order of summation; the add is one
+    IEEE addition per element (inf + -inf is NaN), compared value for value
+    with NaN equal to NaN, under every candidate; padding lanes add nothing."""
+    import torch
+
+    import oracle
+    from paper_2512_22147_amd import datagen, mep
+
+    tdt = torch.float32 if dt == np.float32 else torch.float64
+    code = mep.MEP_F32 if dt == np.float32 else mep.MEP_F64
+    x = datagen.uniform(61 + n, 0, (n,), dt)
+    y = datagen.uniform(61 + n, 1, (n,), dt)
+    x[n - 1] = np.inf
+    if case == "inf-and-neg-inf":
+        x[n // 2] = -np.inf
+        y[n // 2] = np.inf  # the add: -inf + inf at one position
+    elif case == "nan":
+        x[0] = np.nan
+        y[n - 1] = -np.inf  # the add: inf + -inf at the last position
+    want = _sum_class(oracle.reduce_sum(x))
+    assert want == {"inf": 1, "inf-and-neg-inf": 3, "nan": 3}[case]
+
+    def dev(a):
+        raw = torch.empty(n + offset, dtype=tdt, device="cuda:0")
+        raw[offset:].copy_(torch.from_numpy(a))
+        return raw[offset:]
+
+    xd, yd = dev(x), dev(y)
+    for v in [-1] + list(range(mep.mep_variant_count(mep.MEP_OP_REDUCE_SUM, code, 1, n))):
+        mep.mep_set_variant(mep.MEP_OP_REDUCE_SUM, v)
+        got = float(mep.mep_reduce_sum(xd).cpu()[0])
+        assert _sum_class(got) == want, f"sum candidate {v}: {got}"
+    mep.mep_set_variant(mep.MEP_OP_REDUCE_SUM, -1)
+    ref = oracle.vector_add(x, y).astype(dt)
+    for v in [-1] + list(range(mep.mep_variant_count(mep.MEP_OP_VECTOR_ADD, code, 1, n))):
+        mep.mep_set_variant(mep.MEP_OP_VECTOR_ADD, v)
+        c = mep.mep_vector_add(xd, yd)
+        torch.cuda.synchronize()
+        assert np.array_equal(c.cpu().numpy(), ref, equal_nan=True), f"add candidate {v}"
+    mep.mep_set_variant(mep.MEP_OP_VECTOR_ADD, -1)
