@@ -43,9 +43,9 @@
  *   input: every reduction runs in a fixed order and no atomics are used.
  * - NaN and infinities follow IEEE arithmetic on the defining sums: a NaN or
  *   an infinity in an input reaches exactly the outputs whose sums contain
- *   it, and an output is NaN, +inf or -inf exactly where those sums are.
- *   Padding past the end of the matrix adds nothing, even where 0 * inf
- *   would give NaN.
+ *   it, as NaN, +inf or -inf (only where finite partial sums overflow can
+ *   the summation order decide).  Padding past the end of the matrix adds
+ *   nothing, even where 0 * inf would give NaN.
  */
 #ifndef MEP_H
 #define MEP_H
