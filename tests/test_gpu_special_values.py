@@ -23,9 +23,10 @@ pytestmark = pytest.mark.gpu
 # row groups, misaligned rows (element-wise), narrow rows, column panels, one
 # row, where an infinity in the vector gives definite infinities in ATAX's y
 # and GEMVER's x that a padding row of the last block would turn into NaN,
-# and a streamed matrix (past 128 MiB: non-temporal shapes, which skip the
-# rows past the end instead of zeroing them)
-SHAPES = [(1037, 2052), (1001, 2051), (1001, 8), (3, 40001), (1, 4100), (2051, 16384)]
+# a streamed matrix (past 128 MiB: non-temporal shapes, which skip the rows
+# past the end instead of zeroing them), and a streamed one in column panels
+# (with the cyclic, rotated and blocked row maps among its candidates)
+SHAPES = [(1037, 2052), (1001, 2051), (1001, 8), (3, 40001), (1, 4100), (2051, 16384), (1025, 40000)]
 
 # the vector operand multiplied into A, with its length
 VECTOR_IN = {"matvec": ("x", 1), "matvec_t": ("w", 0), "bicg": ("x", 1), "ata_x": ("x", 1),
