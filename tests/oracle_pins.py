@@ -16,7 +16,9 @@ What pins the oracle:
 * closed forms for A = I, A = all-ones, A = diag(d), B = A;
 * integer-valued inputs, whose products and sums are exact in fp64, compared
   bit for bit with numpy's int64 matrix product;
-* numpy's float64 ``@`` as an independent library routine.
+* numpy's float64 ``@`` as an independent library routine;
+* on NaN and infinities, the definitions as plain Python loops over Python
+  floats, which follow IEEE double arithmetic (0 * inf is NaN).
 """
 from __future__ import annotations
 
@@ -350,6 +352,95 @@ def pin_gemver(orc):
     assert np.array_equal(w, 0.5 * float(v1 @ x) * u1)
 
 
+# --- NaN and infinities: brute force over Python floats ---------------------
+
+SV_ALPHA, SV_BETA = 1.5, -0.75
+
+# lists of (operand, position, value); positions are taken modulo the
+# operand's shape.  The last four put an exact zero beside an infinity, so an
+# oracle that skipped zero terms or zero weights (instead of forming
+# 0 * inf = NaN) fails.
+SV_CASES = [[("A", (1, 2), float("nan"))], [("A", (0, 0), float("inf"))], [("A", (2, 3), -float("inf"))],
+            [("B", (1, 1), float("inf"))], [("x", 3, float("inf"))], [("x", 0, float("nan"))],
+            [("w", 1, -float("inf"))], [("u1", 2, float("inf"))], [("v1", 1, -float("inf"))],
+            [("y", 0, float("inf"))], [("z", 2, float("nan"))],
+            [("A", (1, 1), 0.0), ("x", 1, float("inf"))], [("A", (0, 0), 0.0), ("w", 0, float("inf"))],
+            [("A", (1, 2), float("inf")), ("w", 1, 0.0)], [("A", (2, 1), float("inf")), ("x", 1, 0.0)]]
+SV_SHAPES = [(3, 4), (1, 5), (4, 1)]
+
+
+def _sv_class(v):
+    return 3 if v != v else (1 if v == float("inf") else (2 if v == -float("inf") else 0))
+
+
+def _sv_same(got, want, what):
+    got = np.asarray(got, np.float64).ravel()
+    assert got.shape == (len(want),), what
+    for k, (g, w) in enumerate(zip(got.tolist(), want)):
+        assert _sv_class(g) == _sv_class(w), f"{what}[{k}]: {g} vs {w}"
+        if _sv_class(w) == 0:
+            assert abs(g - w) <= 1e-12 * max(1.0, abs(w)), f"{what}[{k}]: {g} vs {w}"
+
+
+def _sv_inputs(case, m, n):
+    rng = np.random.default_rng(7 + m + n)
+    ins = {k: rng.uniform(-1.0, 1.0, shape) for k, shape in
+           (("A", (m, n)), ("B", (m, n)), ("x", (n,)), ("w", (m,)), ("u1", (m,)), ("v1", (n,)), ("u2", (m,)),
+            ("v2", (n,)), ("y", (m,)), ("z", (n,)))}
+    for key, pos, value in case:
+        if ins[key].ndim == 2:
+            ins[key][pos[0] % m, pos[1] % n] = value
+        else:
+            ins[key][pos % ins[key].shape[0]] = value
+    return ins
+
+
+def special_values_case(orc, case, m, n):
+    """Every operation of the oracle on one special-value case, against the
+    definitions as loops over Python floats."""
+    ins = _sv_inputs(case, m, n)
+    A = [[float(v) for v in row] for row in ins["A"]]
+    B = [[float(v) for v in row] for row in ins["B"]]
+    x, w = [float(v) for v in ins["x"]], [float(v) for v in ins["w"]]
+    u1, v1, u2, v2, yv, z = ([float(e) for e in ins[k]] for k in ("u1", "v1", "u2", "v2", "y", "z"))
+
+    def mv(M, v):
+        return [sum(a * b for a, b in zip(row, v)) for row in M]
+
+    def mvt(M, v):
+        return [sum(M[i][j] * v[i] for i in range(len(M))) for j in range(len(M[0]))]
+
+    _sv_same(orc.matvec(ins["A"], ins["x"]), mv(A, x), "matvec")
+    _sv_same(orc.matvec_t(ins["A"], ins["w"]), mvt(A, w), "matvec_t")
+    q, s = orc.bicg(ins["A"], ins["x"], ins["w"])
+    _sv_same(q, mv(A, x), "bicg q")
+    _sv_same(s, mvt(A, w), "bicg s")
+    y, t = orc.ata_x(ins["A"], ins["x"])
+    _sv_same(t, mv(A, x), "ata_x t")
+    _sv_same(y, mvt(A, mv(A, x)), "ata_x y")
+    _sv_same(orc.axpby_mv(SV_ALPHA, ins["A"], SV_BETA, ins["B"], ins["x"]),
+             [SV_ALPHA * a + SV_BETA * b for a, b in zip(mv(A, x), mv(B, x))], "axpby_mv")
+    Ah = [[(A[i][j] + u1[i] * v1[j]) + u2[i] * v2[j] for j in range(n)] for i in range(m)]
+    gx = [SV_BETA * s_ + z[j] for j, s_ in enumerate(mvt(Ah, yv))]
+    gw = [SV_ALPHA * s_ for s_ in mv(Ah, gx)]
+    oA, ox, ow = orc.gemver(SV_ALPHA, SV_BETA, ins["A"], ins["u1"], ins["v1"], ins["u2"], ins["v2"], ins["y"],
+                            ins["z"])
+    _sv_same(oA, [e for row in Ah for e in row], "gemver Ahat")
+    _sv_same(ox, gx, "gemver x")
+    _sv_same(ow, gw, "gemver w")
+
+
+def pin_special_values(orc):
+    for case in SV_CASES:
+        for m, n in SV_SHAPES:
+            special_values_case(orc, case, m, n)
+    for values in ([1.0, float("inf"), 2.0], [float("inf"), -1.0, -float("inf")], [0.5, float("nan"), 1.0]):
+        _sv_same([orc.reduce_sum(np.array(values))], [sum(values)], "reduce_sum")
+        other = [float("inf"), -float("inf"), 0.0]
+        _sv_same(orc.vector_add(np.array(values), np.array(other)), [p + q for p, q in zip(values, other)],
+                 "vector_add")
+
+
 ALL_PINS = [
     pin_bruteforce_matvec,
     pin_bruteforce_matvec_t,
@@ -364,4 +455,5 @@ ALL_PINS = [
     pin_reduce_sum,
     pin_vector_add,
     pin_gemver,
+    pin_special_values,
 ]

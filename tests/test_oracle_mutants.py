@@ -44,6 +44,11 @@ MUTANTS = {
     "gemver_w_from_A": ("oracle_matvec(m, n, Ahat, x, w);", "oracle_matvec(m, n, A, x, w);"),
     "gemver_x_misses_z": ("x[j] = beta * x[j] + z[j];", "x[j] = beta * x[j];"),
     "gemver_swapped_scalars": ("w[i] = alpha * w[i];", "w[i] = beta * w[i];"),
+    # zero terms skipped: the same result on finite inputs, but 0 * inf must give NaN
+    "matvec_skips_zero_elements": ("            acc += A[i * n + j] * x[j];",
+                                   "            if (A[i * n + j] != 0.0) acc += A[i * n + j] * x[j];"),
+    "matvec_t_skips_zero_weights": ("                z[j] += A[i * n + j] * w[i];",
+                                    "                if (w[i] != 0.0) z[j] += A[i * n + j] * w[i];"),
 }
 
 RUNNER = r"""
