@@ -65,14 +65,17 @@ def oracle_outputs(op, ins, dt, alpha=ALPHA, beta=BETA):
 
 
 def gpu_outputs(op, ins, dt, alpha=ALPHA, beta=BETA, dev=None):
-    """Runs op on the GPU and returns host numpy outputs."""
+    """Runs op on the GPU and returns host numpy outputs.  Inputs may be host
+    arrays (copied to the GPU) or tensors already there (used as they are:
+    no operation writes its inputs)."""
     import torch
 
     from paper_2512_22147_amd import mep
 
     dev = dev or torch.device("cuda:0")
-    T = {k: torch.from_numpy(np.ascontiguousarray(v)).to(dev) for k, v in ins.items()}
-    m, n = ins["A"].shape
+    T = {k: v if torch.is_tensor(v) else torch.from_numpy(np.ascontiguousarray(v)).to(dev)
+         for k, v in ins.items()}
+    m, n = T["A"].shape
     if op == "matvec":
         out = {"y": mep.mep_matvec(T["A"], T["x"])}
     elif op == "matvec_t":

@@ -67,6 +67,8 @@ def _inject(op, ins, where):
 def _check_every_candidate(op, ins, dt):
     """The default and every candidate against the oracle: same class at
     every output position, finite outputs within the normwise tolerance."""
+    import torch
+
     from paper_2512_22147_amd import mep
 
     m, n = ins["A"].shape
@@ -75,9 +77,11 @@ def _check_every_candidate(op, ins, dt):
     assert any((c != 0).any() for c in want.values()), "the special value reached no output"
     code = op_code(op)
     count = mep.mep_variant_count(code, mep.MEP_F32 if dt == np.float32 else mep.MEP_F64, m, n)
+    # the inputs go to the GPU once; no operation writes them
+    dins = {k: torch.from_numpy(np.ascontiguousarray(v)).to("cuda:0") for k, v in ins.items()}
     for v in [-1] + list(range(count)):
         mep.mep_set_variant(code, v)
-        got = gpu_outputs(op, ins, dt)
+        got = gpu_outputs(op, dins, dt)
         for k, r in ref.items():
             g = np.asarray(got[k], np.float64).ravel()
             r = np.asarray(r, np.float64).ravel()
