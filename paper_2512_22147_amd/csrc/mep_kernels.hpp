@@ -394,16 +394,18 @@ k_stream(StreamArgs<T> a)
         // holds an infinity, so it must add nothing to the column sums.  Only
         // a block that reaches past the last row (wave-uniform) has such rows.
         const bool tail = blk * BR + BR > row_end;
-        // Streamed instances with row groups of 512 lanes or more and batches
-        // of up to 4 rows skip such rows in the column sums (one row per
-        // wave: a wave-uniform test).  Besides, that branch keeps the column
-        // sums in their registers: without it the compiler copied them once
-        // per batch, and GEMVER's first pass ran 3-7% slower on streamed
-        // matrices (the read-only modes: up to 1.3%).  The other ATAX and
-        // GEMVER instances zero the rows' weights or elements instead: there
-        // the branch cost up to 4% (scalar spills with 8-row batches, shorter
-        // rows and cache-resident matrices).  In A^T w and BICG such rows have
-        // zero weights and zero elements, and add nothing either way.
+        // Instances with non-temporal loads (GEMVER's on streamed matrices;
+        // the read-only modes use them at every size), row groups of 512
+        // lanes or more and batches of up to 4 rows skip such rows in the
+        // column sums (one row per wave: a wave-uniform test).  Besides, that
+        // branch keeps the column sums in their registers: without it the
+        // compiler copied them once per batch, and GEMVER's first pass ran
+        // 3-7% slower on streamed matrices (the read-only modes: up to 1.3%).
+        // The other ATAX and GEMVER instances zero the rows' weights or
+        // elements instead: there the branch cost up to 4% (scalar spills with
+        // 8-row batches, shorter rows and GEMVER's cache-resident matrices).
+        // In A^T w and BICG such rows have zero weights and zero elements, and
+        // add nothing either way.
         constexpr bool SKIP_PAST = WIDE && COL && G >= 512 && B <= 4 && AUX != 0;
         if constexpr (RANK2) {
             // Ahat_i = A_i + u1_i v1 + u2_i v2, in the registers that hold A_i;
