@@ -270,7 +270,8 @@ int mep_variant_count(int op, int dtype, int64_t m, int64_t n);
 int mep_set_variant(int op, int variant);
 /* Writes a short description of candidate `variant` for the shape into buf
  * (at most buf_len bytes, NUL-terminated): lanes per row group, vectors per
- * lane, rows per batch, waves per SIMD, load policy, grid.  Returns MEP_OK,
+ * lane, rows per batch, waves per SIMD, load policy, grid (row workgroups x
+ * column panels).  Returns MEP_OK,
  * or MEP_EINVAL for a bad op, dtype, shape or variant. */
 int mep_variant_info(int op, int dtype, int64_t m, int64_t n, int variant, char* buf, size_t buf_len);
 

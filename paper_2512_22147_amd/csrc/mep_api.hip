@@ -332,6 +332,14 @@ static Plan plan_of(int esize, bool vec, int mode, int64_t m, int64_t n, int cfg
     p.threads = p.c.G < 256 ? 256 : p.c.G;
     p.pw = (int64_t)p.c.G * p.c.V * p.vw;
     p.panels = std::max<int64_t>(1, (n + p.pw - 1) / p.pw);
+    if (p.panels > 1) {
+        // panels of equal width (a multiple of the vector width): a short
+        // last panel would finish early and leave its compute units idle
+        // (8-16% slower for rows of 1.2-2.4 panels)
+        const int64_t even = (n + p.panels - 1) / p.panels;
+        p.pw = std::min<int64_t>(p.pw, (even + p.vw - 1) / p.vw * p.vw);
+        p.panels = (n + p.pw - 1) / p.pw;  // no empty last panel
+    }
     const int64_t rows_per_block = (int64_t)batch_of(p.c.B, mode) * (p.threads / p.c.G);
     const int64_t nblk = (m + rows_per_block - 1) / rows_per_block;
     // enough workgroups to fill the shape's CUX compute units per XCD at its occupancy

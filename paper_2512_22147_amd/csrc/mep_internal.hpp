@@ -112,9 +112,9 @@ struct Plan {
     int cfg;          // index into kVecCfg / kScalarCfg
     Cfg c;
     int threads;      // workgroup size
-    int64_t pw;       // columns per panel
-    int64_t panels;   // column panels (gridDim.y)
-    int64_t nb;       // row workgroups (gridDim.x)
+    int64_t pw;       // columns per panel (equal panels, the last possibly shorter)
+    int64_t panels;   // column panels (gridDim.x)
+    int64_t nb;       // row workgroups (gridDim.y)
 };
 
 // Candidate configurations for an m x n matrix (a pure function of its

@@ -56,7 +56,7 @@ struct StreamArgs {
     const T* x;        // dot vector, length n (x or p)
     const T* w;        // row weights, length m (ATW, BICG)
     T* rowout;         // per-row result, length m (y, q or ATAX's t; may be null for ATAX)
-    T* colpart;        // column partials P[gridDim.x][ldp]
+    T* colpart;        // column partials P[row workgroups][ldp]
     T* dotpart;        // multi-panel: partial dots D[panel][m]
     T* dotpart2;       // multi-panel AXPBY: partial dots of B
     const T* u1;       // rank-2 update (GEMVER): row factors, length m
@@ -67,6 +67,7 @@ struct StreamArgs {
     T alpha, beta;
     int64_t m, n, ldp;
     int blocked;       // row-block map: 0 cyclic, 1 contiguous runs, 2 rotated cyclic (see k_stream)
+    int64_t pw;        // columns per panel (all panels but the last have this width)
     int scale_rows;    // MV: rowout = alpha * dot instead of dot
 };
 
@@ -218,10 +219,15 @@ struct Geometry {
     static constexpr int RPW = G >= 64 ? 1 : 64 / G;  // rows per wave (G < 64)
 };
 
-// The streaming kernel.  Grid: x = row workgroups (rows handed out in
-// blocks of B * RG, block k going to workgroup k mod gridDim.x), y = column
-// panels of width G * V * VW.  Narrow row groups (G < 64) are only launched
-// with a single panel.  WPE is the occupancy target (waves per SIMD), which
+// The streaming kernel.  Grid: x = column panels of a.pw columns (at most
+// G * V * VW; the host makes them equal), y = row workgroups (rows handed out
+// in blocks of B * RG, block k going to row workgroup k mod gridDim.y).
+// Workgroups are dealt to the eight XCDs round-robin by linear id, so with
+// the panel as the fast index the pieces of one row are read on different
+// XCDs; with the panel as the slow index they all went to one XCD, and the
+// panelled shapes streamed 3-22% slower (unequal panels: their short last
+// panel also left compute units idle).  Narrow row groups (G < 64) are only
+// launched with a single panel.  WPE is the occupancy target (waves per SIMD), which
 // sets the register budget per lane to 512 / WPE.
 template <typename T, int VW, int G, int V, int B, int WPE, int MODE, int AUX>
 __global__ void __launch_bounds__(Geometry<G>::THREADS, WPE)
@@ -262,11 +268,13 @@ k_stream(StreamArgs<T> a)
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int64_t m = a.m, n = a.n;
     const int m32 = (int)m;  // the host limits m and n to int range
-    const int64_t col0 = (int64_t)blockIdx.y * PW;
-    const bool multipanel = gridDim.y > 1;
-    const int nbx = gridDim.x;
+    const int bx = (int)blockIdx.y;  // row workgroup
+    const int by = (int)blockIdx.x;  // column panel
+    const int64_t col0 = (int64_t)by * a.pw;
+    const bool multipanel = gridDim.x > 1;
+    const int nbx = gridDim.y;
     // valid bytes of this panel of one row
-    const int64_t pcols = (n - col0) < PW ? (n - col0) : PW;
+    const int64_t pcols = (n - col0) < a.pw ? (n - col0) : a.pw;
     const uint32_t pbytes = (uint32_t)(pcols * ES);
     const int64_t rowbytes = n * ES;
 
@@ -550,9 +558,9 @@ k_stream(StreamArgs<T> a)
                     const int row = blk * BR + j * RG + tid / G;
                     if (row < m32) {
                         if (multipanel) {
-                            a.dotpart[(int64_t)blockIdx.y * m + row] = d[j];
+                            a.dotpart[(int64_t)by * m + row] = d[j];
                             if constexpr (TWO)
-                                a.dotpart2[(int64_t)blockIdx.y * m + row] = d2[j];
+                                a.dotpart2[(int64_t)by * m + row] = d2[j];
                         } else if constexpr (TWO) {
                             a.rowout[row] = fma_t(a.alpha, d[j], a.beta * d2[j]);
                         } else if (a.rowout != nullptr) {
@@ -604,8 +612,8 @@ k_stream(StreamArgs<T> a)
         (void)parity;
     };
 
-    // Row blocks of this workgroup, one per round r (nbx = gridDim.x):
-    // - cyclic (map 0): block blockIdx.x + r * nbx;
+    // Row blocks of this workgroup, one per round r (nbx = gridDim.y):
+    // - cyclic (map 0): block bx + r * nbx;
     // - blocked (map 1): one contiguous run of blocks;
     // - rotated (map 2): round r covers the same window of nbx blocks as the
     //   cyclic map, dealt to the workgroups shifted by r * kRotStride, so that
@@ -622,11 +630,11 @@ k_stream(StreamArgs<T> a)
     int blk0, bstep, bend;
     if (map == 1) {
         const int per = (nblk + nbx - 1) / nbx;
-        blk0 = blockIdx.x * per;
+        blk0 = bx * per;
         bstep = 1;
         bend = blk0 + per < nblk ? blk0 + per : nblk;
     } else {
-        blk0 = blockIdx.x;
+        blk0 = bx;
         bstep = nbx;
         bend = nblk;
     }
@@ -637,7 +645,7 @@ k_stream(StreamArgs<T> a)
         if (map == 2) {
             const unsigned un = (unsigned)nbx;
             const int shift = (int)(((unsigned)r % un) * ((unsigned)kRotStride % un) % un);
-            const int pos = (int)blockIdx.x + shift;
+            const int pos = bx + shift;
             return r * nbx + (pos < nbx ? pos : pos - nbx);
         }
         return blk0 + r * bstep;
@@ -682,7 +690,7 @@ k_stream(StreamArgs<T> a)
     }
 
     if constexpr (COL) {
-        T* out = a.colpart + (int64_t)blockIdx.x * a.ldp + col0;
+        T* out = a.colpart + (int64_t)bx * a.ldp + col0;
         if constexpr (NACCL > 0) {
 #pragma unroll
             for (int k = 0; k < NACCL; ++k)
