@@ -96,6 +96,34 @@ def test_long_rows_use_column_panels(op, dt):
                       what=f"{m}x{n}")
 
 
+# Row lengths around the panel widths (the widest row group covers 32768 fp32
+# or 16384 fp64 elements; GEMVER's first pass half that): just past one panel,
+# three and more panels, odd lengths on the element-wise path.  The host cuts
+# such rows into panels of equal width, a multiple of the vector width, and
+# never leaves the last one empty.
+PANEL_WIDTHS = {np.float32: [16388, 32772, 32769, 65540, 98308, 98307],
+                np.float64: [8194, 16386, 16385, 40002, 49154]}
+
+
+@pytest.mark.parametrize("dt", DTYPES, ids=["f32", "f64"])
+@pytest.mark.parametrize("op", OPS)
+def test_equal_panels_every_candidate(op, dt):
+    from paper_2512_22147_amd import mep
+
+    code = op_code(op)
+    for n in PANEL_WIDTHS[dt]:
+        m = 37
+        ins = make_inputs(op, m, n, dt, seed=300 + n % 1000)
+        ref = oracle_outputs(op, ins, dt)
+        scales = condition_scales(op, ins, dt)
+        count = mep.mep_variant_count(code, mep.MEP_F32 if dt == np.float32 else mep.MEP_F64, m, n)
+        for v in range(count):
+            mep.mep_set_variant(code, v)
+            assert_parity(op, gpu_outputs(op, ins, dt), ref, dt, what=f"{m}x{n} candidate {v}", scales=scales,
+                          dims=(m, n))
+        mep.mep_set_variant(code, -1)
+
+
 @pytest.mark.parametrize("dt", DTYPES, ids=["f32", "f64"])
 @pytest.mark.parametrize("op", OPS)
 def test_misaligned_matrix_takes_elementwise_path(op, dt):
