@@ -278,7 +278,10 @@ int mep_variant_info(int op, int dtype, int64_t m, int64_t n, int variant, char*
 /*
  * One round of the candidate selection of Sec. 3.2 over the library's own
  * kernels for call->op at call's shape: candidate 0 (the default) is the
- * baseline K^(d); every candidate n runs once and its outputs are compared
+ * baseline K^(d).  The default first runs max(8, 2 * warmup) times untimed
+ * (the first launches after an allocation or an idle gap read slower, and
+ * candidate 0 is timed first); then every candidate n runs once and its
+ * outputs are compared
  * with the baseline's by the FE metric of mep_check_fe (Eq. 4, tolerance
  * tol; every output of the call is judged on its own scale, GEMVER's Ahat
  * included, and a non-finite output fails, the baseline's too); each
