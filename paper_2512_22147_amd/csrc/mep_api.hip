@@ -1527,7 +1527,7 @@ int mep_select_variant(const mep_call_t* call, int warmup, int R, int k, int inn
     // Settling runs of the default before any candidate is timed: the first
     // launches after the operands were allocated (or after an idle gap) read
     // a few % slower, and candidate 0, timed first, took that penalty alone
-    // (7% in one round over 4 GiB, which its per-candidate warm-up did not
+    // (7% in one selection over 4 GiB, which its per-candidate warm-up did not
     // absorb).  These runs are not timed and count toward no candidate.
     g_variant[call->op].store(0, std::memory_order_relaxed);
     for (int i = 0; i < std::max(8, 2 * warmup) && rc == MEP_OK; ++i)
